@@ -1,0 +1,188 @@
+/*
+ * fiona.h -- C ABI of the MI355X (gfx950) hybrid weighted sum.
+ *
+ * The operation (Fiona, Sec. 4.2 "Exact Compilation of Routed Linear
+ * Operators", Eq. (routed-example) and Eq. (shared-example)): a routed linear
+ * layer computes every packed output ciphertext y_j from already prepared
+ * (rotated) input ciphertexts A_i as
+ *
+ *     y_j = sum over raw terms (i, pi) of  pt_pi (*) A_i              (one PMult each)
+ *         + sum over signed-sum uses (s, sigma, c) of  c * sigma * U_s
+ *     U_s = sum over members (i, h) of  h * A_i,   h in {-1, 0, +1}   (Add / Sub / skip)
+ *
+ * where (*) is the slot-wise product, c is the reconstruction factor of the
+ * group (applied once to the group's signed sum: "Grouping Reconstruction
+ * Operations"), a signed sum U_s may be shared by several outputs, also with
+ * all signs reversed (sigma = -1: "Sharing Signed Sums"), and the signed and
+ * raw results of an output are added before any rescale ("Combining the
+ * Signed and Raw Routes").  The library evaluates this exactly in every RNS
+ * limb: ciphertexts are in the negacyclic NTT domain, where a PMult is an
+ * element-wise product mod q_l and a constant factor c is a scalar product.
+ * Rotation, key switching, rescale, encoding and bootstrapping are not part
+ * of it.
+ *
+ * Data layout ("limb-major"), all uint64 residues:
+ *   ciphertext i, polynomial p (0 = c0, 1 = c1), limb l, coefficient k is
+ *   element ((i * 2 + p) * L + l) * N + k of a ciphertext array;
+ *   plaintext pi, limb l, coefficient k is element (pi * L + l) * N + k.
+ *
+ * Every function returns FIONA_OK (0) or a negative fiona_status and never
+ * throws or aborts.  All objects are created and destroyed by the caller.
+ */
+#ifndef FIONA_H
+#define FIONA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum fiona_status {
+  FIONA_OK = 0,
+  FIONA_ERR_ARG = -1,          /* null pointer, zero or inconsistent size */
+  FIONA_ERR_PLAN = -2,         /* layer description inconsistent (index out of range, bad CSR) */
+  FIONA_ERR_UNSUPPORTED = -3,  /* N, L or a modulus outside the supported range */
+  FIONA_ERR_ALIGN = -4,        /* a device pointer is not 8-byte aligned */
+  FIONA_ERR_ALIAS = -5,        /* the output buffer overlaps an input buffer */
+  FIONA_ERR_HIP = -6,          /* a HIP runtime call failed (device allocation, copy, launch) */
+  FIONA_ERR_NOMEM = -7,        /* host allocation failed */
+  FIONA_ERR_NODEVICE = -8      /* the plan was created host-only and has no device image */
+} fiona_status;
+
+/* Limits checked by fiona_ctx_create. */
+#define FIONA_MAX_N (1u << 20)
+#define FIONA_MAX_L 64u
+#define FIONA_MODULUS_BITS 50      /* every modulus satisfies 2 <= q < 2^50 */
+#define FIONA_SCALE_BITS 20        /* every integer scale c satisfies c < 2^20 */
+#define FIONA_MAX_MEMBERS 64u      /* longer ternary groups are split into exact sub-sums */
+
+typedef struct fiona_ctx fiona_ctx;
+typedef struct fiona_plan fiona_plan;
+
+/*
+ * fiona_ctx_create: RNS parameters of the ciphertexts.
+ *   N       coefficients per limb, 1 <= N <= FIONA_MAX_N (any N; CKKS uses a
+ *           power of two, and the kernel handles a partial last tile);
+ *   L       number of RNS limbs, 1 <= L <= FIONA_MAX_L;
+ *   moduli  host array of L moduli, each 2 <= q_l < 2^50.  The element-wise
+ *           path does not need them to be NTT-friendly primes; CKKS callers
+ *           pass primes q = 1 (mod 2N).
+ * Host-only: no device memory is touched.  On success *out owns a context
+ * that fiona_ctx_destroy frees.  Errors: FIONA_ERR_ARG (null), FIONA_ERR_UNSUPPORTED.
+ */
+int fiona_ctx_create(uint32_t N, uint32_t L, const uint64_t *moduli, fiona_ctx **out);
+void fiona_ctx_destroy(fiona_ctx *ctx);
+
+/* Plan flags. */
+#define FIONA_PLAN_NO_SHARING 1u   /* evaluate every group's signed sum on its own (no reuse) */
+#define FIONA_PLAN_HOST_ONLY 2u    /* build and check the plan on the host; upload nothing */
+#define FIONA_PLAN_NO_LDS_SUMS 4u  /* never keep shared signed sums resident in LDS */
+
+/*
+ * One routed layer, in the raw per-(output, term) form the offline compiler
+ * emits (paper Sec. 2.2 "Execution Plan": fixed before any query).  Host
+ * arrays, all read during fiona_plan_create only (the caller keeps ownership).
+ *
+ * Raw route, per output CSR:
+ *   pm_off[n_out+1]        terms of output j are pm_off[j] .. pm_off[j+1]-1
+ *   pm_input[n_pm]         input ciphertext of each raw term (< n_in)
+ *   pm_pt[n_pm]            plaintext of each raw term (< n_pt)
+ * Signed route, per output CSR over groups, per group CSR over members:
+ *   grp_off[n_out+1]       groups of output j are grp_off[j] .. grp_off[j+1]-1
+ *   grp_mem_off[n_group+1] members of group g are grp_mem_off[g] .. grp_mem_off[g+1]-1
+ *   mem_input[n_member]    input ciphertext of each member (< n_in)
+ *   mem_sign[n_member]     sign h in {-1, 0, +1} of each member: the same
+ *                          values the caller later passes as ternary_groups
+ *   grp_scale[n_group]     index into the scales array of each group (< n_scale)
+ * n_group and n_member are grp_off[n_out] and grp_mem_off[n_group].
+ */
+typedef struct fiona_layer_desc {
+  uint32_t n_in, n_out, n_pt, n_scale;
+  const uint32_t *pm_off;
+  const uint32_t *pm_input;
+  const uint32_t *pm_pt;
+  const uint32_t *grp_off;
+  const uint32_t *grp_mem_off;
+  const uint32_t *mem_input;
+  const int8_t *mem_sign;
+  const uint32_t *grp_scale;
+  uint32_t flags;
+} fiona_layer_desc;
+
+/*
+ * fiona_plan_create: compile one layer for the GPU.
+ *   - checks every index of desc (FIONA_ERR_PLAN on any inconsistency);
+ *   - drops members whose sign is 0 and groups with no nonzero member: they
+ *     contribute nothing (Sec. 3 Obs. 2, the skip; Sec. 4.2 "contributes nothing");
+ *   - splits groups of more than FIONA_MAX_MEMBERS members into sub-sums with
+ *     the same scale (exact, since c*(U1 + U2) = c*U1 + c*U2);
+ *   - unless FIONA_PLAN_NO_SHARING, finds signed sums that are equal or
+ *     exactly opposite (same inputs, same or all reversed signs) across the
+ *     layer and computes each once (Sec. 4.2 "Sharing Signed Sums"); sums
+ *     used more than once are kept resident in LDS per position tile;
+ *   - uploads the compiled metadata to the current HIP device (synchronous)
+ *     unless FIONA_PLAN_HOST_ONLY.
+ * The plan keeps a reference to ctx (which must outlive it).  Errors:
+ * FIONA_ERR_ARG, FIONA_ERR_PLAN, FIONA_ERR_NOMEM, FIONA_ERR_HIP.
+ */
+int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_plan **out);
+void fiona_plan_destroy(fiona_plan *plan);
+
+/* Operation counts of a compiled plan (per position and polynomial, as the
+ * paper counts CKKS operations per ciphertext in Sec. 4.2 and Sec. 6.2). */
+typedef struct fiona_plan_stats_t {
+  uint64_t ct_terms;               /* all (output, term) pairs, sign-0 members included */
+  uint64_t n_pmult;                /* raw terms: one PMult each */
+  uint64_t n_member;               /* signed terms (members), sign 0 included */
+  uint64_t n_member_nonzero;       /* signed terms with h != 0 */
+  uint64_t n_use;                  /* (output, signed sum) uses: one scalar product each */
+  uint64_t n_sum_distinct;         /* distinct signed sums after sharing */
+  uint64_t n_sum_resident;         /* shared sums kept in LDS, computed once per tile */
+  uint64_t pmult_per_contribution; /* PMults if every signed term were applied on its own */
+  uint64_t pmult_grouped;          /* PMults after grouping: raw terms + uses */
+  uint64_t addsub_unshared;        /* Add/Sub to form every use's signed sum on its own */
+  uint64_t addsub_shared;          /* Add/Sub with each distinct sum formed once */
+  uint32_t tile;                   /* coefficients per workgroup */
+  uint32_t waves;                  /* wavefronts per workgroup */
+  uint32_t lds_bytes;              /* LDS per workgroup */
+  uint32_t grid;                   /* workgroups per launch */
+} fiona_plan_stats_t;
+
+int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);
+
+/*
+ * fiona_hybrid_linear: evaluate the layer (the hot path).
+ *   in_cts          device, [n_in][2][L][N] uint64, every value < 2^50
+ *                   (CKKS residues are < q_l)
+ *   pt_diags        device, [n_pt][L][N] uint64 NTT-domain plaintexts, < 2^50
+ *   ternary_groups  device, [n_member] int8 signs in {-1, 0, +1}, in the
+ *                   member order of the layer description; must equal the
+ *                   mem_sign the plan was created with (members that were 0
+ *                   then are skipped; the others are read here)
+ *   scales          device, [n_scale] uint64 integer reconstruction factors,
+ *                   each < 2^20
+ *   out_cts         device, [n_out][2][L][N] uint64, overwritten with
+ *                   canonical residues in [0, q_l); must not overlap any input
+ *   stream          HIP stream the work is queued on (0 = legacy default)
+ * Asynchronous: returns once the kernel is queued; the buffers must stay
+ * valid and unchanged until the stream reaches it.  Allocates nothing.
+ * Results are exact (bit-identical to evaluating every term on its own mod q_l).
+ * Input ranges above are preconditions that are not checked.  Errors
+ * (nothing is launched): FIONA_ERR_ARG (null pointer with a nonzero size),
+ * FIONA_ERR_ALIGN, FIONA_ERR_ALIAS, FIONA_ERR_NODEVICE, FIONA_ERR_HIP (launch).
+ */
+int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
+                        const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
+                        hipStream_t stream);
+
+/* Static string naming a status code. */
+const char *fiona_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FIONA_H */

@@ -1,0 +1,198 @@
+"""Python binding of the MI355X hybrid weighted sum (include/fiona.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libfiona.so``.  PyTorch supplies device memory and streams.  If
+the library has not been built, importing works but every call raises.
+
+    ctx  = Ctx(N, L, moduli)
+    plan = Plan.from_layer(ctx, layer)          # or Plan(ctx, n_in=..., ...)
+    hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t)
+
+Tensors are device tensors of 8-byte elements (uint64 residues, stored in any
+8-byte dtype) for in/pt/scale/out and int8 for the signs, laid out as the
+header describes: in [n_in][2][L][N], pt [n_pt][L][N], out [n_out][2][L][N].
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfiona.so")
+
+FIONA_PLAN_NO_SHARING = 1
+FIONA_PLAN_HOST_ONLY = 2
+FIONA_PLAN_NO_LDS_SUMS = 4
+
+STATUS = {0: "FIONA_OK", -1: "FIONA_ERR_ARG", -2: "FIONA_ERR_PLAN", -3: "FIONA_ERR_UNSUPPORTED",
+          -4: "FIONA_ERR_ALIGN", -5: "FIONA_ERR_ALIAS", -6: "FIONA_ERR_HIP", -7: "FIONA_ERR_NOMEM",
+          -8: "FIONA_ERR_NODEVICE"}
+
+
+class FionaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (%d)" % (where, STATUS.get(status, "unknown"), status))
+
+
+class _LayerDesc(ctypes.Structure):
+    _fields_ = [("n_in", ctypes.c_uint32), ("n_out", ctypes.c_uint32), ("n_pt", ctypes.c_uint32),
+                ("n_scale", ctypes.c_uint32),
+                ("pm_off", ctypes.c_void_p), ("pm_input", ctypes.c_void_p), ("pm_pt", ctypes.c_void_p),
+                ("grp_off", ctypes.c_void_p), ("grp_mem_off", ctypes.c_void_p),
+                ("mem_input", ctypes.c_void_p), ("mem_sign", ctypes.c_void_p), ("grp_scale", ctypes.c_void_p),
+                ("flags", ctypes.c_uint32)]
+
+
+class _Stats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in (
+        "ct_terms", "n_pmult", "n_member", "n_member_nonzero", "n_use", "n_sum_distinct", "n_sum_resident",
+        "pmult_per_contribution", "pmult_grouped", "addsub_unshared", "addsub_shared")] + \
+        [(n, ctypes.c_uint32) for n in ("tile", "waves", "lds_bytes", "grid")]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libfiona.so is not built (run __graft_entry__.build()); "
+                               "there is no fallback path")
+        L = ctypes.CDLL(LIB_PATH)
+        L.fiona_ctx_create.restype = ctypes.c_int
+        L.fiona_ctx_create.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p,
+                                       ctypes.POINTER(ctypes.c_void_p)]
+        L.fiona_ctx_destroy.restype = None
+        L.fiona_ctx_destroy.argtypes = [ctypes.c_void_p]
+        L.fiona_plan_create.restype = ctypes.c_int
+        L.fiona_plan_create.argtypes = [ctypes.c_void_p, ctypes.POINTER(_LayerDesc),
+                                        ctypes.POINTER(ctypes.c_void_p)]
+        L.fiona_plan_destroy.restype = None
+        L.fiona_plan_destroy.argtypes = [ctypes.c_void_p]
+        L.fiona_plan_stats.restype = ctypes.c_int
+        L.fiona_plan_stats.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Stats)]
+        L.fiona_hybrid_linear.restype = ctypes.c_int
+        L.fiona_hybrid_linear.argtypes = [ctypes.c_void_p] * 7
+        L.fiona_status_string.restype = ctypes.c_char_p
+        L.fiona_status_string.argtypes = [ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str):
+    if rc != 0:
+        raise FionaError(rc, where)
+
+
+class Ctx:
+    """RNS parameters: N coefficients, L limbs with moduli q_l < 2^50."""
+
+    def __init__(self, N: int, L: int, moduli):
+        self.N, self.L = int(N), int(L)
+        self.moduli = [int(q) for q in moduli]
+        arr = (ctypes.c_uint64 * len(self.moduli))(*self.moduli)
+        h = ctypes.c_void_p()
+        _check(lib().fiona_ctx_create(self.N, self.L, ctypes.cast(arr, ctypes.c_void_p), ctypes.byref(h)),
+               "fiona_ctx_create")
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib().fiona_ctx_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _u32(a):
+    return np.ascontiguousarray(a, dtype=np.uint32)
+
+
+class Plan:
+    """A compiled layer (fiona_plan_create)."""
+
+    def __init__(self, ctx: Ctx, n_in, n_out, n_pt, n_scale, pm_off, pm_input, pm_pt, grp_off, grp_mem_off,
+                 mem_input, mem_sign, grp_scale, flags: int = 0):
+        self.ctx = ctx
+        keep = [_u32(pm_off), _u32(pm_input), _u32(pm_pt), _u32(grp_off), _u32(grp_mem_off),
+                _u32(mem_input), np.ascontiguousarray(mem_sign, dtype=np.int8), _u32(grp_scale)]
+
+        def ptr(a):
+            return a.ctypes.data if a.size else None
+
+        d = _LayerDesc(int(n_in), int(n_out), int(n_pt), int(n_scale), *[ptr(a) for a in keep], int(flags))
+        h = ctypes.c_void_p()
+        _check(lib().fiona_plan_create(ctx.handle, ctypes.byref(d), ctypes.byref(h)), "fiona_plan_create")
+        self._h = h
+        self.n_in, self.n_out, self.n_pt, self.n_scale = int(n_in), int(n_out), int(n_pt), int(n_scale)
+        self.n_member = int(keep[4][-1]) if keep[4].size else 0
+
+    @classmethod
+    def from_layer(cls, ctx: Ctx, layer, flags: int = 0) -> "Plan":
+        return cls(ctx, layer.n_in, layer.n_out, layer.n_pt, len(layer.scales), layer.pm_off, layer.pm_input,
+                   layer.pm_pt, layer.grp_off, layer.grp_mem_off, layer.mem_input, layer.mem_sign,
+                   layer.grp_scale, flags)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def stats(self) -> dict:
+        s = _Stats()
+        _check(lib().fiona_plan_stats(self._h, ctypes.byref(s)), "fiona_plan_stats")
+        return {n: int(getattr(s, n)) for n, _ in _Stats._fields_}
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib().fiona_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _dptr(t, name, elem_size):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if t.element_size() != elem_size:
+        raise ValueError("%s must have %d-byte elements" % (name, elem_size))
+    return t.data_ptr()
+
+
+def hybrid_linear(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t, stream=None) -> None:
+    """fiona_hybrid_linear on torch device tensors (queued on ``stream``, default: current)."""
+    import torch
+
+    N, L = plan.ctx.N, plan.ctx.L
+    sizes = [(in_t, "in_cts", plan.n_in * 2 * L * N), (pt_t, "pt_diags", plan.n_pt * L * N),
+             (out_t, "out_cts", plan.n_out * 2 * L * N), (sign_t, "ternary_groups", plan.n_member),
+             (scale_t, "scales", plan.n_scale)]
+    for t, name, n in sizes:
+        if t is not None and t.numel() < n:
+            raise ValueError("%s has %d elements, needs %d" % (name, t.numel(), n))
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    _check(lib().fiona_hybrid_linear(plan.handle, _dptr(in_t, "in_cts", 8), _dptr(pt_t, "pt_diags", 8),
+                                     _dptr(sign_t, "ternary_groups", 1), _dptr(scale_t, "scales", 8),
+                                     _dptr(out_t, "out_cts", 8), s), "fiona_hybrid_linear")

@@ -1,0 +1,394 @@
+// Host side of the C ABI in include/fiona.h: parameter checks, the plan
+// compiler (grouping, sharing, LDS residency) and the kernel launch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <new>
+#include <vector>
+
+#include "fiona.h"
+#include "hybrid_kernel.hpp"
+
+using fiona::KParams;
+using fiona::LimbConst;
+
+namespace {
+
+constexpr int kWaves = 8;                       // wavefronts per workgroup
+constexpr uint32_t kLdsBytes = 160u * 1024u;    // gfx950 LDS per workgroup
+constexpr uint32_t kSlotBytes = fiona::kTile * 16u;   // one input or sum tile in LDS
+constexpr uint32_t kMaxInputs = kLdsBytes / kSlotBytes;
+
+LimbConst make_limb_const(uint64_t q) {
+  LimbConst c;
+  c.q = q;
+  c.r50 = (uint64_t)((((unsigned __int128)1) << 50) % q);
+  c.r50_shoup = (uint64_t)((((unsigned __int128)c.r50) << 64) / q);
+  c.qinv = 1.0 / (double)q;
+  return c;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool ranges_overlap(const void *a, size_t na, const void *b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+}  // namespace
+
+struct fiona_ctx {
+  uint32_t N = 0, L = 0;
+  std::vector<uint64_t> q;
+  std::vector<LimbConst> limbs;
+};
+
+struct fiona_plan {
+  const fiona_ctx *ctx = nullptr;
+  uint32_t n_in = 0, n_out = 0, n_pt = 0, n_scale = 0, n_member_desc = 0;
+  uint32_t n_mat = 0;
+  uint32_t flags = 0;
+  fiona_plan_stats_t st{};
+  std::vector<uint4> outs;
+  std::vector<uint2> pm;
+  std::vector<uint4> uses;
+  std::vector<uint2> mats;
+  std::vector<uint2> members;
+  void *dev = nullptr;
+  int device = -1;
+  KParams kp{};
+  uint32_t lds_bytes = 0, grid = 0, tiles = 0;
+  bool any_signed = false;
+};
+
+extern "C" {
+
+const char *fiona_status_string(int status) {
+  switch (status) {
+    case FIONA_OK: return "ok";
+    case FIONA_ERR_ARG: return "invalid argument";
+    case FIONA_ERR_PLAN: return "inconsistent layer description";
+    case FIONA_ERR_UNSUPPORTED: return "unsupported size or modulus";
+    case FIONA_ERR_ALIGN: return "device pointer not 8-byte aligned";
+    case FIONA_ERR_ALIAS: return "output overlaps an input";
+    case FIONA_ERR_HIP: return "HIP runtime error";
+    case FIONA_ERR_NOMEM: return "out of host memory";
+    case FIONA_ERR_NODEVICE: return "plan has no device image";
+    default: return "unknown status";
+  }
+}
+
+int fiona_ctx_create(uint32_t N, uint32_t L, const uint64_t *moduli, fiona_ctx **out) {
+  if (!out) return FIONA_ERR_ARG;
+  *out = nullptr;
+  if (!moduli) return FIONA_ERR_ARG;
+  if (N == 0 || N > FIONA_MAX_N || L == 0 || L > FIONA_MAX_L) return FIONA_ERR_UNSUPPORTED;
+  for (uint32_t l = 0; l < L; ++l)
+    if (moduli[l] < 2 || moduli[l] >= (1ull << FIONA_MODULUS_BITS)) return FIONA_ERR_UNSUPPORTED;
+  fiona_ctx *c = new (std::nothrow) fiona_ctx;
+  if (!c) return FIONA_ERR_NOMEM;
+  try {
+    c->N = N;
+    c->L = L;
+    c->q.assign(moduli, moduli + L);
+    for (uint32_t l = 0; l < L; ++l) c->limbs.push_back(make_limb_const(moduli[l]));
+  } catch (...) {
+    delete c;
+    return FIONA_ERR_NOMEM;
+  }
+  *out = c;
+  return FIONA_OK;
+}
+
+void fiona_ctx_destroy(fiona_ctx *ctx) { delete ctx; }
+
+}  // extern "C"
+
+namespace {
+
+// Checks every index of the description (no partial trust).
+int validate_desc(const fiona_layer_desc *d) {
+  if (!d->pm_off || !d->grp_off) return FIONA_ERR_ARG;
+  if (d->n_in == 0) return FIONA_ERR_ARG;
+  if (d->n_out >= (1u << 30) || d->n_pt >= (1u << 31) || d->n_scale >= (1u << 31)) return FIONA_ERR_PLAN;
+  if (d->pm_off[0] != 0 || d->grp_off[0] != 0) return FIONA_ERR_PLAN;
+  for (uint32_t j = 0; j < d->n_out; ++j)
+    if (d->pm_off[j + 1] < d->pm_off[j] || d->grp_off[j + 1] < d->grp_off[j]) return FIONA_ERR_PLAN;
+  const uint32_t n_pm = d->pm_off[d->n_out];
+  const uint32_t n_group = d->grp_off[d->n_out];
+  if (n_pm && (!d->pm_input || !d->pm_pt)) return FIONA_ERR_ARG;
+  for (uint32_t t = 0; t < n_pm; ++t)
+    if (d->pm_input[t] >= d->n_in || d->pm_pt[t] >= d->n_pt) return FIONA_ERR_PLAN;
+  if (n_group) {
+    if (!d->grp_mem_off || !d->grp_scale) return FIONA_ERR_ARG;
+    if (d->grp_mem_off[0] != 0) return FIONA_ERR_PLAN;
+    for (uint32_t g = 0; g < n_group; ++g) {
+      if (d->grp_mem_off[g + 1] < d->grp_mem_off[g]) return FIONA_ERR_PLAN;
+      if (d->grp_scale[g] >= d->n_scale) return FIONA_ERR_PLAN;
+    }
+    const uint32_t n_member = d->grp_mem_off[n_group];
+    if (n_member >= (1u << 31)) return FIONA_ERR_PLAN;
+    if (n_member && (!d->mem_input || !d->mem_sign)) return FIONA_ERR_ARG;
+    for (uint32_t m = 0; m < n_member; ++m) {
+      if (d->mem_input[m] >= d->n_in) return FIONA_ERR_PLAN;
+      if (d->mem_sign[m] < -1 || d->mem_sign[m] > 1) return FIONA_ERR_PLAN;
+    }
+  }
+  return FIONA_OK;
+}
+
+struct SumBuild {
+  std::vector<uint2> members;  // (input, index into the sign array) of the representative
+  bool flip = false;           // representative's canonicalisation flipped its signs
+  uint32_t n_use = 0;
+  uint32_t slot = fiona::kInlineSum;
+  uint32_t mem_begin = 0;
+};
+
+int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
+  const bool share = !(d->flags & FIONA_PLAN_NO_SHARING);
+  const uint32_t n_pm = d->pm_off[d->n_out];
+  const uint32_t n_group = d->grp_off[d->n_out];
+  P->n_member_desc = n_group ? d->grp_mem_off[n_group] : 0;
+
+  std::vector<SumBuild> sums;
+  std::map<std::vector<uint64_t>, uint32_t> index;   // canonical signed sum -> sum id
+  struct Use { uint32_t sum, scale; bool neg; };
+  std::vector<std::vector<Use>> out_uses(d->n_out);
+
+  uint64_t nz_members = 0, addsub_unshared = 0;
+  for (uint32_t j = 0; j < d->n_out; ++j) {
+    for (uint32_t g = d->grp_off[j]; g < d->grp_off[j + 1]; ++g) {
+      // nonzero members of the group, split into sub-sums of at most kMaxMembers
+      std::vector<std::pair<uint64_t, uint32_t>> nz;   // (input*2 + negative, member index)
+      for (uint32_t m = d->grp_mem_off[g]; m < d->grp_mem_off[g + 1]; ++m) {
+        if (d->mem_sign[m] == 0) continue;
+        nz.push_back({(uint64_t)d->mem_input[m] * 2 + (d->mem_sign[m] < 0 ? 1 : 0), m});
+      }
+      nz_members += nz.size();
+      for (size_t c0 = 0; c0 < nz.size(); c0 += fiona::kMaxMembers) {
+        const size_t c1 = std::min(nz.size(), c0 + (size_t)fiona::kMaxMembers);
+        std::vector<std::pair<uint64_t, uint32_t>> part(nz.begin() + c0, nz.begin() + c1);
+        std::sort(part.begin(), part.end());
+        const bool flip = (part[0].first & 1) != 0;   // canonical form: first member positive
+        std::vector<uint64_t> key(part.size());
+        for (size_t t = 0; t < part.size(); ++t) key[t] = part[t].first ^ (flip ? 1 : 0);
+        addsub_unshared += part.size() - 1;
+        uint32_t sid;
+        auto it = share ? index.find(key) : index.end();
+        if (it == index.end()) {
+          sid = (uint32_t)sums.size();
+          SumBuild sb;
+          sb.flip = flip;
+          for (auto &pr : part) sb.members.push_back(make_uint2((uint32_t)(pr.first >> 1), pr.second));
+          sums.push_back(std::move(sb));
+          if (share) index.emplace(std::move(key), sid);
+        } else {
+          sid = it->second;
+        }
+        sums[sid].n_use++;
+        out_uses[j].push_back(Use{sid, d->grp_scale[g], flip != sums[sid].flip});
+      }
+    }
+  }
+
+  // LDS residency for sums used more than once, most used first
+  const bool lds_sums = !(d->flags & FIONA_PLAN_NO_LDS_SUMS);
+  std::vector<uint32_t> cand;
+  for (uint32_t s = 0; s < sums.size(); ++s)
+    if (lds_sums && sums[s].n_use >= 2) cand.push_back(s);
+  std::stable_sort(cand.begin(), cand.end(),
+                   [&](uint32_t a, uint32_t b) { return sums[a].n_use > sums[b].n_use; });
+  const uint32_t max_slots = kMaxInputs - d->n_in;
+  if (cand.size() > max_slots) cand.resize(max_slots);
+
+  // device records
+  uint64_t addsub_shared = 0;
+  for (auto &sb : sums) {
+    sb.mem_begin = (uint32_t)P->members.size();
+    for (auto &m : sb.members) P->members.push_back(m);
+    addsub_shared += sb.members.size() - 1;
+  }
+  for (uint32_t s : cand) {
+    sums[s].slot = (uint32_t)P->mats.size();
+    P->mats.push_back(make_uint2(sums[s].mem_begin, (uint32_t)sums[s].members.size()));
+  }
+  P->n_mat = (uint32_t)P->mats.size();
+  for (uint32_t j = 0; j < d->n_out; ++j) {
+    const uint32_t pb = d->pm_off[j], pc = d->pm_off[j + 1] - pb;
+    const uint32_t ub = (uint32_t)P->uses.size();
+    for (const Use &u : out_uses[j]) {
+      const SumBuild &sb = sums[u.sum];
+      P->uses.push_back(make_uint4(sb.mem_begin, (uint32_t)sb.members.size(), sb.slot,
+                                   u.scale | (u.neg ? 0x80000000u : 0u)));
+    }
+    P->outs.push_back(make_uint4(pb, pc, ub, (uint32_t)out_uses[j].size()));
+  }
+  for (uint32_t t = 0; t < n_pm; ++t) P->pm.push_back(make_uint2(d->pm_pt[t], d->pm_input[t]));
+
+  fiona_plan_stats_t &st = P->st;
+  st.n_pmult = n_pm;
+  st.n_member = P->n_member_desc;
+  st.ct_terms = (uint64_t)n_pm + P->n_member_desc;
+  st.n_member_nonzero = nz_members;
+  st.n_use = P->uses.size();
+  st.n_sum_distinct = sums.size();
+  st.n_sum_resident = P->n_mat;
+  st.pmult_per_contribution = (uint64_t)n_pm + nz_members;
+  st.pmult_grouped = (uint64_t)n_pm + P->uses.size();
+  st.addsub_unshared = addsub_unshared;
+  st.addsub_shared = addsub_shared;
+  P->any_signed = !P->uses.empty();
+  return FIONA_OK;
+}
+
+int upload_plan(fiona_plan *P) {
+  const fiona_ctx *C = P->ctx;
+  const size_t a = 256;
+  const size_t o_limbs = 0;
+  const size_t o_outs = align_up(o_limbs + sizeof(LimbConst) * C->L, a);
+  const size_t o_pm = align_up(o_outs + sizeof(uint4) * P->outs.size(), a);
+  const size_t o_uses = align_up(o_pm + sizeof(uint2) * P->pm.size(), a);
+  const size_t o_mats = align_up(o_uses + sizeof(uint4) * P->uses.size(), a);
+  const size_t o_mem = align_up(o_mats + sizeof(uint2) * P->mats.size(), a);
+  const size_t total = align_up(o_mem + sizeof(uint2) * P->members.size(), a);
+  std::vector<unsigned char> host(total, 0);
+  auto put = [&](size_t off, const void *src, size_t n) { if (n) std::memcpy(host.data() + off, src, n); };
+  put(o_limbs, C->limbs.data(), sizeof(LimbConst) * C->L);
+  put(o_outs, P->outs.data(), sizeof(uint4) * P->outs.size());
+  put(o_pm, P->pm.data(), sizeof(uint2) * P->pm.size());
+  put(o_uses, P->uses.data(), sizeof(uint4) * P->uses.size());
+  put(o_mats, P->mats.data(), sizeof(uint2) * P->mats.size());
+  put(o_mem, P->members.data(), sizeof(uint2) * P->members.size());
+  if (hipGetDevice(&P->device) != hipSuccess) return FIONA_ERR_HIP;
+  if (hipMalloc(&P->dev, total) != hipSuccess) {
+    P->dev = nullptr;
+    return FIONA_ERR_HIP;
+  }
+  if (hipMemcpy(P->dev, host.data(), total, hipMemcpyHostToDevice) != hipSuccess) return FIONA_ERR_HIP;
+  static bool attr_set = false;
+  if (!attr_set) {
+    if (hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<kWaves>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes) != hipSuccess)
+      return FIONA_ERR_HIP;
+    attr_set = true;
+  }
+  unsigned char *base = (unsigned char *)P->dev;
+  KParams &k = P->kp;
+  k.limbs = (const LimbConst *)(base + o_limbs);
+  k.outs = (const uint4 *)(base + o_outs);
+  k.pm = (const uint2 *)(base + o_pm);
+  k.uses = (const uint4 *)(base + o_uses);
+  k.mats = (const uint2 *)(base + o_mats);
+  k.members = (const uint2 *)(base + o_mem);
+  return FIONA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_plan **out) {
+  if (!out) return FIONA_ERR_ARG;
+  *out = nullptr;
+  if (!ctx || !desc) return FIONA_ERR_ARG;
+  int rc = validate_desc(desc);
+  if (rc != FIONA_OK) return rc;
+  if (desc->n_in > kMaxInputs) return FIONA_ERR_UNSUPPORTED;
+  fiona_plan *P = new (std::nothrow) fiona_plan;
+  if (!P) return FIONA_ERR_NOMEM;
+  P->ctx = ctx;
+  P->n_in = desc->n_in;
+  P->n_out = desc->n_out;
+  P->n_pt = desc->n_pt;
+  P->n_scale = desc->n_scale;
+  P->flags = desc->flags;
+  try {
+    rc = compile_plan(P, desc);
+  } catch (...) {
+    rc = FIONA_ERR_NOMEM;
+  }
+  if (rc != FIONA_OK) {
+    delete P;
+    return rc;
+  }
+  P->tiles = (ctx->N + fiona::kTile - 1) / fiona::kTile;
+  P->grid = P->tiles * ctx->L;
+  P->lds_bytes = (P->n_in + P->n_mat) * kSlotBytes;
+  P->st.tile = fiona::kTile;
+  P->st.waves = kWaves;
+  P->st.lds_bytes = P->lds_bytes;
+  P->st.grid = P->grid;
+  KParams &k = P->kp;
+  k.N = ctx->N;
+  k.L = ctx->L;
+  k.n_in = P->n_in;
+  k.n_out = P->n_out;
+  k.n_mat = P->n_mat;
+  k.tiles = P->tiles;
+  if (!(desc->flags & FIONA_PLAN_HOST_ONLY)) {
+    rc = upload_plan(P);
+    if (rc != FIONA_OK) {
+      fiona_plan_destroy(P);
+      return rc;
+    }
+  }
+  *out = P;
+  return FIONA_OK;
+}
+
+void fiona_plan_destroy(fiona_plan *plan) {
+  if (!plan) return;
+  if (plan->dev) (void)hipFree(plan->dev);
+  delete plan;
+}
+
+int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out) {
+  if (!plan || !out) return FIONA_ERR_ARG;
+  *out = plan->st;
+  return FIONA_OK;
+}
+
+int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
+                        const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
+                        hipStream_t stream) {
+  if (!plan) return FIONA_ERR_ARG;
+  if (!plan->dev) return FIONA_ERR_NODEVICE;
+  const fiona_ctx *C = plan->ctx;
+  const size_t LN = (size_t)C->L * C->N;
+  const size_t in_bytes = (size_t)plan->n_in * 2 * LN * 8;
+  const size_t pt_bytes = (size_t)plan->n_pt * LN * 8;
+  const size_t out_bytes = (size_t)plan->n_out * 2 * LN * 8;
+  const size_t sign_bytes = plan->n_member_desc;
+  const size_t scale_bytes = (size_t)plan->n_scale * 8;
+  if (!in_cts) return FIONA_ERR_ARG;
+  if (plan->n_out && !out_cts) return FIONA_ERR_ARG;
+  if (!plan->pm.empty() && !pt_diags) return FIONA_ERR_ARG;
+  if (plan->any_signed && (!ternary_groups || !scales)) return FIONA_ERR_ARG;
+  if (((uintptr_t)in_cts | (uintptr_t)pt_diags | (uintptr_t)scales | (uintptr_t)out_cts) & 7u)
+    return FIONA_ERR_ALIGN;
+  if (ranges_overlap(out_cts, out_bytes, in_cts, in_bytes) ||
+      ranges_overlap(out_cts, out_bytes, pt_diags, pt_bytes) ||
+      ranges_overlap(out_cts, out_bytes, ternary_groups, sign_bytes) ||
+      ranges_overlap(out_cts, out_bytes, scales, scale_bytes))
+    return FIONA_ERR_ALIAS;
+  if (plan->n_out == 0) return FIONA_OK;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return FIONA_ERR_ARG;
+  KParams k = plan->kp;
+  k.in = in_cts;
+  k.pt = pt_diags;
+  k.signs = ternary_groups;
+  k.scales = scales;
+  k.out = out_cts;
+  hipLaunchKernelGGL(fiona::hybrid_linear_kernel<kWaves>, dim3(plan->grid), dim3(kWaves * 64),
+                     plan->lds_bytes, stream, k);
+  if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
+  return FIONA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,177 @@
+"""C-ABI checks that need no GPU: exported symbols, argument and plan
+validation, and the plan compiler's grouping/sharing counts (host-only plans)."""
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+import paper_2609_35352_amd as fiona
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+HOST = fiona.FIONA_PLAN_HOST_ONLY
+
+pytestmark = pytest.mark.skipif(not os.path.exists(fiona.LIB_PATH), reason="libfiona.so not built")
+
+
+def _declared_functions(path):
+    src = open(path).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(fiona_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions(os.path.join(ROOT, "include", "fiona.h"))
+    assert set(names) >= {"fiona_ctx_create", "fiona_ctx_destroy", "fiona_plan_create", "fiona_plan_destroy",
+                          "fiona_plan_stats", "fiona_hybrid_linear", "fiona_status_string"}
+    lib = ctypes.CDLL(fiona.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_synth_library_exports():
+    import synth.gpu
+    if not os.path.exists(synth.gpu.LIB_PATH):
+        pytest.skip("synth library not built")
+    lib = ctypes.CDLL(synth.gpu.LIB_PATH)
+    assert hasattr(lib, "synth_fill_uniform") and hasattr(lib, "synth_fill_pts")
+
+
+def test_status_strings():
+    L = fiona.lib()
+    for code in range(-8, 1):
+        assert L.fiona_status_string(code)
+    assert L.fiona_status_string(0) == b"ok"
+
+
+def test_ctx_validation():
+    q = synth.ntt_primes(1 << 12, 2)
+    fiona.Ctx(1 << 12, 2, q).close()
+    for N, L, mods, status in [(0, 2, q, -3), (1 << 21, 2, q, -3), (4096, 0, q, -3), (4096, 65, q * 40, -3),
+                               (4096, 2, [q[0], 1 << 50], -3), (4096, 2, [q[0], 1], -3)]:
+        with pytest.raises(fiona.FionaError) as e:
+            fiona.Ctx(N, L, mods)
+        assert e.value.status == status
+    h = ctypes.c_void_p()
+    assert fiona.lib().fiona_ctx_create(16, 1, None, ctypes.byref(h)) == -1
+
+
+def _small_layer(**kw):
+    cfg = synth.LayerConfig("t", N=256, L=2, n_in=16, n_out=6, T=32, g=8, ternary=0.5, **kw)
+    return synth.make_layer(cfg, 3, moduli=synth.ntt_primes(256, 2))
+
+
+def _plan_args(layer):
+    return dict(n_in=layer.n_in, n_out=layer.n_out, n_pt=layer.n_pt, n_scale=len(layer.scales),
+                pm_off=layer.pm_off, pm_input=layer.pm_input, pm_pt=layer.pm_pt, grp_off=layer.grp_off,
+                grp_mem_off=layer.grp_mem_off, mem_input=layer.mem_input, mem_sign=layer.mem_sign,
+                grp_scale=layer.grp_scale)
+
+
+def test_plan_validation_errors():
+    lay = _small_layer()
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    ok = _plan_args(lay)
+    fiona.Plan(ctx, flags=HOST, **ok).close()
+    bad_cases = []
+    a = dict(ok); a["pm_input"] = ok["pm_input"].copy(); a["pm_input"][3] = lay.n_in; bad_cases.append(a)
+    a = dict(ok); a["pm_pt"] = ok["pm_pt"].copy(); a["pm_pt"][0] = lay.n_pt; bad_cases.append(a)
+    a = dict(ok); a["mem_input"] = ok["mem_input"].copy(); a["mem_input"][1] = 999; bad_cases.append(a)
+    a = dict(ok); a["mem_sign"] = ok["mem_sign"].copy(); a["mem_sign"][2] = 2; bad_cases.append(a)
+    a = dict(ok); a["grp_scale"] = ok["grp_scale"].copy(); a["grp_scale"][0] = len(lay.scales); bad_cases.append(a)
+    a = dict(ok); a["pm_off"] = ok["pm_off"].copy(); a["pm_off"][2], a["pm_off"][3] = a["pm_off"][3], a["pm_off"][2]
+    bad_cases.append(a)
+    a = dict(ok); a["grp_mem_off"] = ok["grp_mem_off"].copy(); a["grp_mem_off"][0] = 1; bad_cases.append(a)
+    for a in bad_cases:
+        with pytest.raises(fiona.FionaError) as e:
+            fiona.Plan(ctx, flags=HOST, **a)
+        assert e.value.status == -2
+    a = dict(ok); a["n_in"] = 0
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.Plan(ctx, flags=HOST, **a)
+    assert e.value.status == -1
+    a = dict(ok); a["n_in"] = 161
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.Plan(ctx, flags=HOST, **a)
+    assert e.value.status == -3
+
+
+def test_hybrid_linear_error_paths_without_device():
+    lay = _small_layer()
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    plan = fiona.Plan(ctx, flags=HOST, **_plan_args(lay))
+    L = fiona.lib()
+    assert L.fiona_hybrid_linear(None, None, None, None, None, None, None) == -1
+    # host-only plan: refused before any pointer is used
+    assert L.fiona_hybrid_linear(plan.handle, 8, 8, 8, 8, 16, None) == -8
+
+
+def test_worked_example_counts():
+    """Sec. 4.2: 7 PMults term by term, 5 after grouping, one Sub saved by sharing U = A1 - A3."""
+    ex = json.load(open(os.path.join(GOLDEN, "routed_example.json")))
+    pm_off, pm_in, pm_pt, gm_off, m_in, m_sg = [0], [], [], [0], [], []
+    for o in ex["outputs"]:
+        for i, _ in o["raw"]:
+            pm_in.append(i)
+            pm_pt.append(len(pm_pt))
+        pm_off.append(len(pm_in))
+        for i, h in o["signed"]["members"]:
+            m_in.append(i)
+            m_sg.append(h)
+        gm_off.append(len(m_in))
+    q = synth.ntt_primes(16, 1)
+    ctx = fiona.Ctx(16, 1, q)
+    args = dict(n_in=ex["n_in"], n_out=2, n_pt=len(pm_pt), n_scale=2, pm_off=pm_off, pm_input=pm_in, pm_pt=pm_pt,
+                grp_off=[0, 1, 2], grp_mem_off=gm_off, mem_input=m_in, mem_sign=m_sg, grp_scale=[0, 1])
+    st = fiona.Plan(ctx, flags=HOST, **args).stats()
+    assert st["pmult_per_contribution"] == ex["pmult_per_contribution"] == 7
+    assert st["pmult_grouped"] == ex["pmult_grouped"] == 5
+    assert st["addsub_unshared"] - st["addsub_shared"] == ex["addsub_saved_by_sharing"] == 1
+    assert st["n_sum_distinct"] == 1 and st["n_use"] == 2 and st["n_sum_resident"] == 1
+    assert st["ct_terms"] == 8 and st["n_member_nonzero"] == 4
+    st2 = fiona.Plan(ctx, flags=HOST | fiona.FIONA_PLAN_NO_SHARING, **args).stats()
+    assert st2["n_sum_distinct"] == 2 and st2["addsub_shared"] == st2["addsub_unshared"] == 2
+    assert st2["pmult_grouped"] == 5
+
+
+def test_sharing_finds_opposite_sums():
+    # output 0: A0 - A1 + A2 ; output 1: -A0 + A1 - A2 (all reversed) ; output 2: A2 + A1 - A0 (other order)
+    q = synth.ntt_primes(16, 1)
+    ctx = fiona.Ctx(16, 1, q)
+    args = dict(n_in=3, n_out=3, n_pt=0, n_scale=3, pm_off=[0, 0, 0, 0], pm_input=[], pm_pt=[],
+                grp_off=[0, 1, 2, 3], grp_mem_off=[0, 3, 6, 9], mem_input=[0, 1, 2, 0, 1, 2, 2, 1, 0],
+                mem_sign=[1, -1, 1, -1, 1, -1, 1, -1, 1], grp_scale=[0, 1, 2])
+    st = fiona.Plan(ctx, flags=HOST, **args).stats()
+    # the third sum is A2 - A1 + A0 = the first one
+    assert st["n_sum_distinct"] == 1 and st["n_use"] == 3
+    assert st["addsub_unshared"] == 6 and st["addsub_shared"] == 2
+
+
+def test_long_groups_are_split_and_zero_groups_dropped():
+    q = synth.ntt_primes(16, 1)
+    ctx = fiona.Ctx(16, 1, q)
+    n = 150
+    args = dict(n_in=150, n_out=2, n_pt=0, n_scale=2, pm_off=[0, 0, 0], pm_input=[], pm_pt=[],
+                grp_off=[0, 1, 2], grp_mem_off=[0, n, n + 4], mem_input=list(range(n)) + [0, 1, 2, 3],
+                mem_sign=[1] * n + [0, 0, 0, 0], grp_scale=[0, 1])
+    st = fiona.Plan(ctx, flags=HOST, **args).stats()
+    assert st["n_use"] == 3            # ceil(150 / 64) sub-sums; the all-zero group contributes nothing
+    assert st["n_member_nonzero"] == 150 and st["n_member"] == 154
+    assert st["pmult_grouped"] == 3 and st["pmult_per_contribution"] == 150
+
+
+@pytest.mark.parametrize("name", ["vgg11", "vit768", "bert_ffn"])
+def test_config_plans(name):
+    lay = synth.make_layer(synth.CONFIGS[name], 1)
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    st = fiona.Plan.from_layer(ctx, lay, flags=HOST).stats()
+    assert st["ct_terms"] == lay.ct_terms and st["n_pmult"] == lay.n_pm
+    assert st["pmult_grouped"] == lay.n_pm + st["n_use"]
+    if name == "vit768":
+        assert st["n_sum_distinct"] <= 48 and st["n_sum_resident"] == st["n_sum_distinct"]
+    assert st["grid"] == lay.L * lay.N // 64
+    assert st["lds_bytes"] == (lay.n_in + st["n_sum_resident"]) * 1024 <= 160 * 1024

@@ -1,0 +1,302 @@
+"""GPU parity: the HIP path against the oracle, through the C ABI.
+
+Small layers are compared element by element (every output, polynomial, limb
+and coefficient); the full-size layers run in the same launch configuration
+as the benchmark, on device-generated inputs, and are compared at sampled
+positions that the oracle computes from the same generator.  Every comparison
+is bit-exact.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+import paper_2609_35352_amd as fiona
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    # fail loudly if the native library is missing: there is no other path
+    fiona.lib()
+    import synth.gpu
+    synth.gpu.lib()
+    return torch.device("cuda:0")
+
+
+def _to_dev(a, dtype, dev):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).view(dtype)).to(dev)
+
+
+def _run(layer, dev, x=None, pt=None, flags=0, scales=None, signs=None):
+    """Run the layer on the GPU; x/pt from host arrays or, if None, filled on the device."""
+    import torch
+    import synth.gpu
+    N, L = layer.N, layer.L
+    ctx = fiona.Ctx(N, L, layer.moduli)
+    plan = fiona.Plan.from_layer(ctx, layer, flags=flags)
+    if x is None:
+        in_t = torch.empty(layer.n_in * 2 * L * N, dtype=torch.int64, device=dev)
+        synth.gpu.fill_inputs(layer, in_t)
+    else:
+        in_t = _to_dev(x, np.int64, dev)
+    if pt is None:
+        pt_t = torch.empty(max(1, layer.n_pt * L * N), dtype=torch.int64, device=dev)
+        synth.gpu.fill_pts(layer, pt_t)
+    else:
+        pt_t = _to_dev(pt, np.int64, dev) if pt.size else torch.zeros(1, dtype=torch.int64, device=dev)
+    sg = layer.mem_sign if signs is None else signs
+    sign_t = _to_dev(sg, np.int8, dev) if sg.size else torch.zeros(1, dtype=torch.int8, device=dev)
+    sc = layer.scales if scales is None else scales
+    scale_t = _to_dev(sc, np.int64, dev) if sc.size else torch.zeros(1, dtype=torch.int64, device=dev)
+    out_t = torch.full((max(1, layer.n_out * 2 * L * N),), -1, dtype=torch.int64, device=dev)
+    fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t)
+    torch.cuda.synchronize()
+    return out_t, in_t, pt_t, plan
+
+
+def _host(out_t, layer):
+    return out_t.cpu().numpy().view(np.uint64)[: layer.n_out * 2 * layer.L * layer.N].reshape(
+        layer.n_out, 2, layer.L, layer.N)
+
+
+def _assert_equal(got, expect, what):
+    bad = np.argwhere(got != expect)
+    if bad.size:
+        first = tuple(int(v) for v in bad[0])
+        raise AssertionError("%s: %d mismatches; first at (out, poly, limb, coeff) = %s: gpu %d, oracle %d"
+                             % (what, len(bad), first, got[first], expect[first]))
+
+
+SMALL = {
+    "tiny": synth.CONFIGS["tiny"],
+    "ragged_pool": synth.LayerConfig("ragged_pool", N=1000, L=3, n_in=24, n_out=7, T=48, g=8, ternary=0.5, pool=4),
+    "many_outputs": synth.LayerConfig("many_outputs", N=197, L=2, n_in=16, n_out=37, T=16, g=4, ternary=0.4),
+    "fold_raw": synth.LayerConfig("fold_raw", N=128, L=2, n_in=8, n_out=3, T=2600, g=8, ternary=0.3),
+    "fold_uses": synth.LayerConfig("fold_uses", N=64, L=2, n_in=8, n_out=2, T=4400, g=1, ternary=0.6),
+    "big_groups": synth.LayerConfig("big_groups", N=256, L=2, n_in=100, n_out=3, T=400, g=100, ternary=0.5),
+    "lds_full": synth.LayerConfig("lds_full", N=128, L=1, n_in=160, n_out=4, T=320, g=32, ternary=0.5, pool=2),
+    "all_ternary": synth.LayerConfig("all_ternary", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=1.0, pool=3),
+    "all_raw": synth.LayerConfig("all_raw", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=0.0),
+}
+
+
+def _small_layer(name):
+    cfg = SMALL[name]
+    if name == "tiny":
+        return synth.make_layer(cfg, 1)
+    Nq = 1 << max(6, (cfg.N - 1).bit_length())
+    return synth.make_layer(cfg, 5, moduli=synth.ntt_primes(Nq, cfg.L))
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_layer_elementwise(dev, name):
+    layer = _small_layer(name)
+    _say("[parity] %s: N=%d L=%d n_in=%d n_out=%d terms/out=%d" % (name, layer.N, layer.L, layer.n_in,
+                                                                   layer.n_out, layer.cfg.T))
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    out_t, *_ = _run(layer, dev, x, pt)
+    _assert_equal(_host(out_t, layer), expect, name)
+
+
+@pytest.mark.parametrize("flags", [fiona.FIONA_PLAN_NO_SHARING, fiona.FIONA_PLAN_NO_LDS_SUMS,
+                                   fiona.FIONA_PLAN_NO_SHARING | fiona.FIONA_PLAN_NO_LDS_SUMS])
+def test_plan_variants_agree(dev, flags):
+    layer = _small_layer("ragged_pool")
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    out_t, *_ = _run(layer, dev, x, pt, flags=flags)
+    _assert_equal(_host(out_t, layer), expect, "flags=%d" % flags)
+
+
+def test_seeds_2_and_3_tiny(dev):
+    for seed in (2, 3):
+        layer = synth.make_layer(synth.CONFIGS["tiny"], seed)
+        x, pt = synth.input_values(layer), synth.pt_values(layer)
+        out_t, *_ = _run(layer, dev, x, pt)
+        _assert_equal(_host(out_t, layer), oracle.weighted_sum_layer(layer, x, pt), "tiny seed %d" % seed)
+
+
+def test_boundary_values(dev):
+    """Largest residues everywhere: inputs and plaintexts q-1, scales 2^20-1."""
+    layer = _small_layer("ragged_pool")
+    q = np.asarray(layer.moduli, np.uint64)
+    x = np.broadcast_to((q - 1)[None, None, :, None], (layer.n_in, 2, layer.L, layer.N)).copy()
+    pt = np.broadcast_to((q - 1)[None, :, None], (layer.n_pt, layer.L, layer.N)).copy()
+    scales = np.full(len(layer.scales), (1 << 20) - 1, np.uint64)
+    lay2 = synth.Layer(**{**layer.__dict__, "scales": scales})
+    expect = oracle.weighted_sum_layer(lay2, x, pt)
+    out_t, *_ = _run(lay2, dev, x, pt)
+    _assert_equal(_host(out_t, lay2), expect, "q-1 everywhere")
+    # zeros everywhere
+    out_t, *_ = _run(lay2, dev, np.zeros_like(x), np.zeros_like(pt))
+    assert (_host(out_t, lay2) == 0).all()
+
+
+def test_outputs_without_terms(dev):
+    q = synth.ntt_primes(128, 1)
+    cfg = synth.LayerConfig("empty", N=128, L=1, n_in=3, n_out=3, T=0, g=1, ternary=0.0)
+    layer = synth.Layer(cfg=cfg, moduli=q, seed=1, n_in=3, n_out=3, out_global=np.arange(3, dtype=np.uint32),
+                        pm_off=np.array([0, 0, 1, 1], np.uint32), pm_input=np.array([2], np.uint32),
+                        pm_pt=np.array([0], np.uint32), grp_off=np.array([0, 0, 0, 1], np.uint32),
+                        grp_mem_off=np.array([0, 2], np.uint32), mem_input=np.array([0, 1], np.uint32),
+                        mem_sign=np.array([0, 0], np.int8), grp_scale=np.array([0], np.uint32),
+                        scales=np.array([5], np.uint64), pt_global=np.arange(1, dtype=np.uint64))
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    out_t, *_ = _run(layer, dev, x, pt)
+    got = _host(out_t, layer)
+    _assert_equal(got, oracle.weighted_sum_layer(layer, x, pt), "empty outputs")
+    assert (got[0] == 0).all() and (got[2] == 0).all()
+
+
+def test_ntt_domain_product_is_ring_product(dev):
+    """GPU PMult on NTT(a), NTT(b) at N = 64..256 equals the schoolbook negacyclic product."""
+    for N in (64, 256):
+        q = synth.ntt_primes(1 << 12, 2)
+        psi = [oracle.find_psi(N, qq) for qq in q]
+        rng = np.random.default_rng(N)
+        a = [rng.integers(0, qq, N, dtype=np.uint64) for qq in q]
+        b = [rng.integers(0, qq, N, dtype=np.uint64) for qq in q]
+        A = np.stack([oracle.ntt(a[l], q[l], psi[l]) for l in range(2)])
+        B = np.stack([oracle.ntt(b[l], q[l], psi[l]) for l in range(2)])
+        cfg = synth.LayerConfig("ring", N=N, L=2, n_in=1, n_out=1, T=1, g=1, ternary=0.0)
+        layer = synth.Layer(cfg=cfg, moduli=q, seed=1, n_in=1, n_out=1, out_global=np.arange(1, dtype=np.uint32),
+                            pm_off=np.array([0, 1], np.uint32), pm_input=np.array([0], np.uint32),
+                            pm_pt=np.array([0], np.uint32), grp_off=np.array([0, 0], np.uint32),
+                            grp_mem_off=np.array([0], np.uint32), mem_input=np.zeros(0, np.uint32),
+                            mem_sign=np.zeros(0, np.int8), grp_scale=np.zeros(0, np.uint32),
+                            scales=np.zeros(0, np.uint64), pt_global=np.arange(1, dtype=np.uint64))
+        x = np.stack([A, A])[None]
+        out_t, *_ = _run(layer, dev, x, B[None])
+        got = _host(out_t, layer)
+        for l in range(2):
+            assert (oracle.intt(got[0, 0, l], q[l], psi[l]) == oracle.negacyclic_mul(a[l], b[l], q[l])).all()
+
+
+def test_toy_ckks_on_gpu(dev):
+    from oracle import ckks_toy
+    layer = synth.make_layer(synth.CONFIGS["tiny"], 1)
+    toy, x, w, cts, pts, expected = ckks_toy.build_toy(layer)
+    out_t, *_ = _run(layer, dev, cts, pts)
+    got = _host(out_t, layer)
+    _assert_equal(got, oracle.weighted_sum_layer(layer, cts, pts), "toy ckks")
+    dec = np.stack([toy.decrypt(got[j]) for j in range(layer.n_out)])
+    err = ckks_toy.relative_error(dec, expected)
+    _say("[parity] toy CKKS decode relative error %.3g" % err)
+    assert err <= 1e-3
+
+
+def test_device_generator_matches_numpy(dev):
+    import torch
+    import synth.gpu
+    cfg = synth.LayerConfig("gen", N=1000, L=3, n_in=5, n_out=2, T=10, g=5, ternary=0.5)
+    layer = synth.make_layer(cfg, 9, moduli=synth.ntt_primes(1024, 3))
+    in_t = torch.empty(layer.n_in * 2 * cfg.L * cfg.N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_inputs(layer, in_t)
+    pt_t = torch.empty(layer.n_pt * cfg.L * cfg.N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_pts(layer, pt_t)
+    torch.cuda.synchronize()
+    assert (in_t.cpu().numpy().view(np.uint64).reshape(layer.n_in, 2, cfg.L, cfg.N) == synth.input_values(layer)).all()
+    assert (pt_t.cpu().numpy().view(np.uint64).reshape(layer.n_pt, cfg.L, cfg.N) == synth.pt_values(layer)).all()
+    allpm = synth.all_pmult_layer(layer)
+    pa_t = torch.empty(allpm.n_pt * cfg.L * cfg.N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_pts(allpm, pa_t)
+    torch.cuda.synchronize()
+    assert (pa_t.cpu().numpy().view(np.uint64).reshape(allpm.n_pt, cfg.L, cfg.N) == synth.pt_values(allpm)).all()
+
+
+# ---------------------------------------------------------------------------
+# Full-size layers, sampled positions
+# ---------------------------------------------------------------------------
+
+def _check_sampled(layer, out_t, in_t, n_samples, seed, what):
+    limbs, coeffs = synth.sample_positions(layer.N, layer.L, n_samples, seed)
+    x_s = synth.input_values(layer, (limbs, coeffs))
+    pt_s = synth.pt_values(layer, (limbs, coeffs)) if layer.n_pt else np.zeros((0, len(limbs)), np.uint64)
+    # the device-filled inputs at these positions are the generator's values
+    xin = in_t.view(layer.n_in, 2, layer.L, layer.N)[:, :, limbs, coeffs].cpu().numpy().view(np.uint64)
+    assert (xin == x_s).all(), "device input generator disagrees with NumPy"
+    expect = oracle.weighted_sum_sampled(layer, limbs, coeffs, x_s, pt_s, n_threads=16)
+    got = out_t[: layer.n_out * 2 * layer.L * layer.N].view(layer.n_out, 2, layer.L, layer.N)[
+        :, :, limbs, coeffs].cpu().numpy().view(np.uint64)
+    bad = np.argwhere(got != expect)
+    if bad.size:
+        j, p, s = (int(v) for v in bad[0])
+        raise AssertionError("%s: %d mismatches; first at out %d poly %d limb %d coeff %d: gpu %d oracle %d"
+                             % (what, len(bad), j, p, limbs[s], coeffs[s], got[j, p, s], expect[j, p, s]))
+
+
+@pytest.mark.parametrize("name", ["vgg11", "vit768", "bert_ffn"])
+def test_full_size_sampled(dev, name):
+    import torch
+    layer = synth.make_layer(synth.CONFIGS[name], 1)
+    _say("[parity] %s full size: %d outputs, %d raw terms, %d groups" % (name, layer.n_out, layer.n_pm,
+                                                                        layer.n_group))
+    out_t, in_t, pt_t, plan = _run(layer, dev)
+    _say("[parity] %s kernel done, plan %s" % (name, plan.stats()))
+    del pt_t
+    _check_sampled(layer, out_t, in_t, 48, 100, name)
+    del out_t, in_t
+    torch.cuda.empty_cache()
+
+
+def test_full_size_large_all_chunks(dev):
+    import torch
+    import synth.gpu
+    layer = synth.make_layer(synth.CONFIGS["large4096"], 1)
+    in_t = torch.empty(layer.n_in * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_inputs(layer, in_t)
+    limbs, coeffs = synth.sample_positions(layer.N, layer.L, 24, 101)
+    x_s = synth.input_values(layer, (limbs, coeffs))
+    chunks = synth.output_chunks(layer.n_out, layer.cfg.chunks_hybrid)
+    max_pt = max(synth.chunk_layer(layer, a, b).n_pt for a, b in chunks)
+    pt_t = torch.empty(max_pt * layer.L * layer.N, dtype=torch.int64, device=dev)
+    out_c = torch.empty((layer.n_out // len(chunks) + 1) * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    sign_all = _to_dev(layer.mem_sign, np.int8, dev)
+    for ci, (a, b) in enumerate(chunks):
+        ch = synth.chunk_layer(layer, a, b)
+        synth.gpu.fill_pts(ch, pt_t)
+        plan = fiona.Plan.from_layer(ctx, ch)
+        sign_t = _to_dev(ch.mem_sign, np.int8, dev)
+        scale_t = _to_dev(ch.scales, np.int64, dev)
+        fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_c)
+        torch.cuda.synchronize()
+        if ci % 4 == 0 or ci == len(chunks) - 1:
+            _say("[parity] large4096 chunk %d/%d (outputs %d..%d) done" % (ci + 1, len(chunks), a, b - 1))
+        pt_s = synth.pt_values(ch, (limbs, coeffs))
+        expect = oracle.weighted_sum_sampled(ch, limbs, coeffs, x_s, pt_s, n_threads=16)
+        got = out_c[: ch.n_out * 2 * layer.L * layer.N].view(ch.n_out, 2, layer.L, layer.N)[
+            :, :, limbs, coeffs].cpu().numpy().view(np.uint64)
+        assert (got == expect).all(), "large4096 chunk %d mismatch" % ci
+    del pt_t, out_c, in_t, sign_all
+    torch.cuda.empty_cache()
+
+
+def test_full_size_all_pmult_route_equivalence(dev):
+    """VGG11-like layer: the all-PMult layer gives exactly the hybrid outputs at every position."""
+    import torch
+    layer = synth.make_layer(synth.CONFIGS["vgg11"], 1)
+    out_h, in_t, pt_t, _ = _run(layer, dev)
+    del pt_t
+    allpm = synth.all_pmult_layer(layer)
+    out_a, in_a, pt_a, _ = _run(allpm, dev)
+    del pt_a, in_a
+    assert torch.equal(out_h, out_a)
+    _check_sampled(allpm, out_a, in_t, 16, 102, "vgg11 all-PMult")
+    del out_h, out_a, in_t
+    torch.cuda.empty_cache()
