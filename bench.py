@@ -1,0 +1,241 @@
+"""Benchmark of the hybrid weighted sum on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config vgg11] [--no-cpu-baseline]
+
+A step is one fiona_hybrid_linear call over the whole layer (every output,
+both polynomials, every limb and coefficient), inputs already resident in HBM.
+The default workload is the VGG11-like 3x3 conv layer (N=2^16, L=8, 64 input
+ciphertexts, 128 outputs x 64 terms, 53% ternary in groups of 8).  The same
+layer is also timed with every term as a PMult (all-PMult), which computes the
+identical outputs, for the speedup of the hybrid route.  Layers whose
+plaintext table exceeds the per-chunk budget run in output chunks (plaintexts
+regenerated on the device between chunks, untimed) and the chunk times add up.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, vendor peak
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("fiona.hip", "hybrid_kernel.hpp", "modarith.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_35352_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, variant: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source; else None."""
+    path = os.path.join(PROFILE_DIR, "hbm_traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_src_sha") != kernel_source_hash():
+        return None
+    v = rec.get(variant)
+    return None if v is None else float(v["bytes_per_launch"])
+
+
+def time_layer(layer, dev, steps, warmup, stream, label):
+    """Run every output chunk of `layer`; return (sum of per-chunk ms per launch, bytes, kernel list)."""
+    import torch
+    import synth
+    import synth.gpu
+    import paper_2609_35352_amd as fiona
+
+    cfg = layer.cfg
+    n_chunks = cfg.chunks_hybrid if layer.pt_const is None else cfg.chunks_allpm
+    chunks = synth.output_chunks(layer.n_out, n_chunks)
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    in_t = torch.empty(layer.n_in * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_inputs(layer, in_t)
+    subs = [synth.chunk_layer(layer, a, b) for a, b in chunks]
+    max_pt = max(max(1, s.n_pt) for s in subs)
+    max_out = max(s.n_out for s in subs)
+    pt_t = torch.empty(max_pt * layer.L * layer.N, dtype=torch.int64, device=dev)
+    out_t = torch.empty(max_out * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    total_ms = 0.0
+    total_bytes = 0
+    per_chunk = []
+    for ci, sub in enumerate(subs):
+        synth.gpu.fill_pts(sub, pt_t)
+        plan = fiona.Plan.from_layer(ctx, sub)
+        sign_t = torch.from_numpy(np.ascontiguousarray(sub.mem_sign)).to(dev) if sub.mem_sign.size else \
+            torch.zeros(1, dtype=torch.int8, device=dev)
+        scale_t = torch.from_numpy(np.ascontiguousarray(sub.scales.view(np.int64))).to(dev) if sub.scales.size \
+            else torch.zeros(1, dtype=torch.int64, device=dev)
+        torch.cuda.synchronize()
+        for _ in range(warmup):
+            fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        nbytes = synth.algorithmic_bytes(sub)
+        total_ms += ms
+        total_bytes += nbytes
+        per_chunk.append({"outputs": sub.n_out, "ms": round(ms, 4), "alg_GBps": round(nbytes / ms / 1e6, 1)})
+        if ci == 0 or ci == len(subs) - 1 or ci % 8 == 0:
+            log("[bench] %s chunk %d/%d: %.3f ms/launch, %.1f GB/s algorithmic, plan %s"
+                % (label, ci + 1, len(subs), ms, nbytes / ms / 1e6, plan.stats()))
+        del plan
+    del pt_t, out_t, in_t
+    torch.cuda.empty_cache()
+    return total_ms, total_bytes, per_chunk
+
+
+def cpu_baseline(layer, seconds: float = 10.0):
+    """The oracle (test infrastructure, plain C) on a bounded sample of the same layer."""
+    import oracle
+    import synth
+
+    threads = min(os.cpu_count() or 1, 16)
+    S = 2048
+    limbs, coeffs = synth.sample_positions(layer.N, layer.L, S, 7)
+    x_s = synth.input_values(layer, (limbs, coeffs))
+    pt_s = synth.pt_values(layer, (limbs, coeffs))
+    n_pos = len(limbs)
+    passes, t = 0, 0.0
+    while t < seconds and passes < 1000:
+        t0 = time.perf_counter()
+        oracle.weighted_sum_sampled(layer, limbs, coeffs, x_s, pt_s, n_threads=threads)
+        t += time.perf_counter() - t0
+        passes += 1
+    frac = n_pos / float(layer.L * layer.N)
+    value = layer.ct_terms * frac * passes / t
+    return {"value": value, "unit": "ct-terms/s", "cores": threads, "kind": "oracle",
+            "sample": "%d (limb, coeff) positions of the layer x all %d outputs x %d terms x 2 polys, %d passes "
+                      "in %.1f s (inputs generated before timing)" % (n_pos, layer.n_out, layer.cfg.T, passes, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="vgg11")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-allpmult", action="store_true", help="time only the hybrid layer")
+    ap.add_argument("--only-allpmult", action="store_true", help="time only the all-PMult layer")
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="only copy 4 GiB device-to-device (torch copy kernel) to calibrate HBM counters")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build measures one GPU only; the hybrid weighted sum has no "
+              "multi-GPU path here (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2609_35352_amd as fiona
+
+    if args.calib_copy:
+        n = 1 << 29   # 4 GiB of int64
+        a = torch.ones(n, dtype=torch.int64, device="cuda:0")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calib_copy_bytes_read": n * 8, "calib_copy_bytes_written": n * 8, "launches": 3}))
+        return
+
+    if not os.path.exists(fiona.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    fiona.lib()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=dev)   # default priority
+    cfg = synth.CONFIGS[args.config]
+    layer = synth.make_layer(cfg, args.seed)
+    log("[bench] %s: %s" % (cfg.name, cfg.description))
+
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    if args.only_allpmult:
+        apl = synth.all_pmult_layer(layer)
+        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult")
+        print(json.dumps({"variant": "all-PMult", "workload": cfg.name, "ms_per_step": round(ap_ms, 4),
+                          "value": round(layer.ct_terms / (ap_ms * 1e-3), 1), "unit": "ct-terms/s",
+                          "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "chunks": ap_chunks}), flush=True)
+        return
+    hy_ms, hy_bytes, hy_chunks = time_layer(layer, dev, args.steps, args.warmup, stream, "hybrid")
+    torch.cuda.synchronize()
+    hy_value = layer.ct_terms / (hy_ms * 1e-3)
+    hy_gbs = hy_bytes / hy_ms / 1e6
+
+    allpm = None
+    if not args.no_allpmult:
+        apl = synth.all_pmult_layer(layer)
+        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult")
+        allpm = {"value": round(layer.ct_terms / (ap_ms * 1e-3), 1), "ms_per_step": round(ap_ms, 4),
+                 "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "alg_bytes": ap_bytes,
+                 "frac_of_hbm_peak": round(ap_bytes / ap_ms / 1e6 / HBM_PEAK_GBS, 4),
+                 "chunks": len(ap_chunks), "speedup_hybrid_vs_allpmult": round(ap_ms / hy_ms, 3)}
+    wall = time.perf_counter() - t_wall0
+
+    traffic = measured_traffic(cfg.name, "hybrid")
+    n_launch = len(hy_chunks)
+    result = {
+        "metric": "ct-terms/sec and achieved HBM GB/s (hybrid vs all-PMult), N=2^16 layers, 1 GPU",
+        "value": round(hy_value, 1),
+        "unit": "ct-terms/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(hy_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic (seeded counter-based generator, uniform residues; no dataset or weights)",
+        "config": {"workload": "%s: %s" % (cfg.name, cfg.description), "N": cfg.N, "L": cfg.L,
+                   "n_in": cfg.n_in, "n_out": cfg.n_out, "terms_per_output": cfg.T, "group": cfg.g,
+                   "ternary_groups": layer.n_group, "raw_terms": layer.n_pm, "ct_terms": layer.ct_terms,
+                   "chunks": n_launch, "seed": args.seed},
+        "achieved_alg_GBps": round(hy_gbs, 1),
+        "roofline": {"bound": "hbm", "achieved": round(hy_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(hy_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None if traffic is None else round(traffic),
+                     "alg_bytes_per_launch": hy_bytes // n_launch,
+                     "kernel": "hybrid_linear_kernel<8>"},
+        "all_pmult": allpm,
+        "hybrid_chunks": hy_chunks if n_launch > 1 else None,
+        "gpu_wall_s": round(wall, 2),
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample (about 10 s)")
+        result["cpu_baseline"] = cpu_baseline(layer)
+        result["cpu_baseline"]["value"] = round(result["cpu_baseline"]["value"], 1)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
