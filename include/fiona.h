@@ -58,6 +58,8 @@ typedef enum fiona_status {
 #define FIONA_MODULUS_BITS 50      /* every modulus satisfies 2 <= q < 2^50 */
 #define FIONA_SCALE_BITS 20        /* every integer scale c satisfies c < 2^20 */
 #define FIONA_MAX_MEMBERS 64u      /* longer ternary groups are split into exact sub-sums */
+#define FIONA_MAX_INPUTS 159u      /* input ciphertexts per layer: a 64-coefficient tile of every
+                                      input (16 B each) plus one zero row fill the 160 KiB LDS */
 
 typedef struct fiona_ctx fiona_ctx;
 typedef struct fiona_plan fiona_plan;
@@ -126,7 +128,10 @@ typedef struct fiona_layer_desc {
  *   - uploads the compiled metadata to the current HIP device (synchronous)
  *     unless FIONA_PLAN_HOST_ONLY.
  * The plan keeps a reference to ctx (which must outlive it).  Errors:
- * FIONA_ERR_ARG, FIONA_ERR_PLAN, FIONA_ERR_NOMEM, FIONA_ERR_HIP.
+ * FIONA_ERR_ARG, FIONA_ERR_PLAN, FIONA_ERR_UNSUPPORTED (more than FIONA_MAX_INPUTS
+ * inputs), FIONA_ERR_NOMEM, FIONA_ERR_HIP.  The plan owns a small device
+ * workspace (the members of its signed sums, reordered by sign on every call),
+ * so one plan must not be used by two streams at the same time.
  */
 int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_plan **out);
 void fiona_plan_destroy(fiona_plan *plan);
@@ -149,6 +154,8 @@ typedef struct fiona_plan_stats_t {
   uint32_t waves;                  /* wavefronts per workgroup */
   uint32_t lds_bytes;              /* LDS per workgroup */
   uint32_t grid;                   /* workgroups per launch */
+  uint32_t split_outputs;          /* outputs split into segments over several wavefronts */
+  uint32_t segment_slots;          /* LDS rows holding the segments' partial residues */
 } fiona_plan_stats_t;
 
 int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);

@@ -50,7 +50,7 @@ class _Stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "ct_terms", "n_pmult", "n_member", "n_member_nonzero", "n_use", "n_sum_distinct", "n_sum_resident",
         "pmult_per_contribution", "pmult_grouped", "addsub_unshared", "addsub_shared")] + \
-        [(n, ctypes.c_uint32) for n in ("tile", "waves", "lds_bytes", "grid")]
+        [(n, ctypes.c_uint32) for n in ("tile", "waves", "lds_bytes", "grid", "split_outputs", "segment_slots")]
 
 
 _lib = None

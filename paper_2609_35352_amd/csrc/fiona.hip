@@ -17,10 +17,17 @@ using fiona::LimbConst;
 
 namespace {
 
-constexpr int kWaves = 8;                       // wavefronts per workgroup
-constexpr uint32_t kLdsBytes = 160u * 1024u;    // gfx950 LDS per workgroup
+constexpr uint32_t kLdsBytes = 160u * 1024u;    // gfx950 LDS per workgroup (and per CU)
 constexpr uint32_t kSlotBytes = fiona::kTile * 16u;   // one input or sum tile in LDS
-constexpr uint32_t kMaxInputs = kLdsBytes / kSlotBytes;
+constexpr uint32_t kMaxInputs = kLdsBytes / kSlotBytes;   // LDS rows of one workgroup
+static_assert(FIONA_MAX_INPUTS + 1 == kMaxInputs, "inputs plus the zero row fill the LDS");
+constexpr uint32_t kMaxSegments = 64;           // segments of one split output
+// Relative costs used to balance work items over wavefronts (units: one raw term).
+constexpr double kCostUseResident = 0.6;
+constexpr double kCostUseInline = 0.5;
+constexpr double kCostMember = 0.25;
+constexpr double kCostFinish = 6.0;
+constexpr double kMinSegmentCost = 128.0;
 
 LimbConst make_limb_const(uint64_t q) {
   LimbConst c;
@@ -53,11 +60,16 @@ struct fiona_plan {
   uint32_t n_mat = 0;
   uint32_t flags = 0;
   fiona_plan_stats_t st{};
-  std::vector<uint4> outs;
+  std::vector<uint4> items;
+  std::vector<uint32_t> dest;
+  std::vector<uint2> waves;
+  std::vector<uint4> splits;
+  uint32_t nw = 8, n_seg_slots = 0;
   std::vector<uint2> pm;
   std::vector<uint4> uses;
   std::vector<uint2> mats;
   std::vector<uint2> members;
+  std::vector<uint2> sums_dev;
   void *dev = nullptr;
   int device = -1;
   KParams kp{};
@@ -196,21 +208,56 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
     }
   }
 
-  // LDS residency for sums used more than once, most used first
+  // Candidates for LDS residency: sums used more than once, most used first.
   const bool lds_sums = !(d->flags & FIONA_PLAN_NO_LDS_SUMS);
   std::vector<uint32_t> cand;
   for (uint32_t s = 0; s < sums.size(); ++s)
     if (lds_sums && sums[s].n_use >= 2) cand.push_back(s);
   std::stable_sort(cand.begin(), cand.end(),
                    [&](uint32_t a, uint32_t b) { return sums[a].n_use > sums[b].n_use; });
-  const uint32_t max_slots = kMaxInputs - d->n_in;
-  if (cand.size() > max_slots) cand.resize(max_slots);
+  const uint32_t lds_free = kMaxInputs - d->n_in - 1;   // slots left after the inputs and the zero row
+  // One workgroup per CU when the LDS image exceeds half the CU: then 16 wavefronts.
+  const uint32_t est_slots = d->n_in + std::min<uint32_t>((uint32_t)cand.size(), lds_free);
+  P->nw = est_slots * 2 > kMaxInputs ? 16 : 8;
+  std::vector<char> resident(sums.size(), 0);
+  for (size_t c = 0; c < cand.size() && c < lds_free; ++c) resident[cand[c]] = 1;
 
-  // device records
+  // Work items: whole outputs, or segments of outputs that are long compared
+  // with the share of one wavefront.
+  auto use_cost = [&](const Use &u) {
+    return resident[u.sum] ? kCostUseResident
+                           : kCostUseInline + kCostMember * (double)sums[u.sum].members.size();
+  };
+  std::vector<double> out_cost(d->n_out);
+  double total = 0;
+  for (uint32_t j = 0; j < d->n_out; ++j) {
+    double c = kCostFinish + (double)(d->pm_off[j + 1] - d->pm_off[j]);
+    for (const Use &u : out_uses[j]) c += use_cost(u);
+    out_cost[j] = c;
+    total += c;
+  }
+  const double target = total / P->nw;
+  std::vector<uint32_t> nseg(d->n_out, 1);
+  uint32_t seg_slots = 0;
+  for (uint32_t j = 0; j < d->n_out; ++j) {
+    if (out_cost[j] <= 1.25 * target) continue;
+    uint32_t S = (uint32_t)(out_cost[j] / target + 0.5);
+    S = std::min<uint32_t>(S, (uint32_t)(out_cost[j] / kMinSegmentCost));
+    S = std::min<uint32_t>(S, kMaxSegments);
+    if (S >= 2 && seg_slots + S <= lds_free) {
+      nseg[j] = S;
+      seg_slots += S;
+    }
+  }
+  P->n_seg_slots = seg_slots;
+  if (cand.size() > lds_free - seg_slots) cand.resize(lds_free - seg_slots);
+
+  // device records: members of every distinct sum, resident sums, uses per output
   uint64_t addsub_shared = 0;
   for (auto &sb : sums) {
     sb.mem_begin = (uint32_t)P->members.size();
     for (auto &m : sb.members) P->members.push_back(m);
+    P->sums_dev.push_back(make_uint2(sb.mem_begin, (uint32_t)sb.members.size()));
     addsub_shared += sb.members.size() - 1;
   }
   for (uint32_t s : cand) {
@@ -218,17 +265,55 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
     P->mats.push_back(make_uint2(sums[s].mem_begin, (uint32_t)sums[s].members.size()));
   }
   P->n_mat = (uint32_t)P->mats.size();
+  std::vector<uint32_t> use_begin(d->n_out);
   for (uint32_t j = 0; j < d->n_out; ++j) {
-    const uint32_t pb = d->pm_off[j], pc = d->pm_off[j + 1] - pb;
-    const uint32_t ub = (uint32_t)P->uses.size();
+    use_begin[j] = (uint32_t)P->uses.size();
     for (const Use &u : out_uses[j]) {
       const SumBuild &sb = sums[u.sum];
       P->uses.push_back(make_uint4(sb.mem_begin, (uint32_t)sb.members.size(), sb.slot,
                                    u.scale | (u.neg ? 0x80000000u : 0u)));
     }
-    P->outs.push_back(make_uint4(pb, pc, ub, (uint32_t)out_uses[j].size()));
   }
   for (uint32_t t = 0; t < n_pm; ++t) P->pm.push_back(make_uint2(d->pm_pt[t], d->pm_input[t]));
+
+  // items, each with its cost; segments of a split output get consecutive LDS slots
+  struct Item { uint4 rec; uint32_t dest; double cost; };
+  std::vector<Item> items;
+  uint32_t slot = 0;
+  for (uint32_t j = 0; j < d->n_out; ++j) {
+    const uint32_t pb = d->pm_off[j], pc = d->pm_off[j + 1] - pb;
+    const uint32_t ub = use_begin[j], uc = (uint32_t)out_uses[j].size();
+    const uint32_t S = nseg[j];
+    if (S > 1) P->splits.push_back(make_uint4(j, slot, S, 0));
+    for (uint32_t g = 0; g < S; ++g) {
+      const uint32_t r0 = (uint32_t)((uint64_t)pc * g / S), r1 = (uint32_t)((uint64_t)pc * (g + 1) / S);
+      const uint32_t u0 = (uint32_t)((uint64_t)uc * g / S), u1 = (uint32_t)((uint64_t)uc * (g + 1) / S);
+      double c = kCostFinish + (double)(r1 - r0);
+      for (uint32_t u = u0; u < u1; ++u) c += use_cost(out_uses[j][u]);
+      items.push_back(Item{make_uint4(pb + r0, r1 - r0, ub + u0, u1 - u0),
+                           S > 1 ? (fiona::kSegmentFlag | (slot + g)) : j, c});
+    }
+    if (S > 1) slot += S;
+  }
+  // longest item first onto the least loaded wavefront
+  std::vector<uint32_t> order(items.size());
+  for (uint32_t t = 0; t < order.size(); ++t) order[t] = t;
+  std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return items[a].cost > items[b].cost; });
+  std::vector<double> load(P->nw, 0.0);
+  std::vector<std::vector<uint32_t>> per_wave(P->nw);
+  for (uint32_t t : order) {
+    const uint32_t w = (uint32_t)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[w] += items[t].cost;
+    per_wave[w].push_back(t);
+  }
+  for (uint32_t w = 0; w < P->nw; ++w) {
+    std::sort(per_wave[w].begin(), per_wave[w].end());
+    P->waves.push_back(make_uint2((uint32_t)P->items.size(), (uint32_t)per_wave[w].size()));
+    for (uint32_t t : per_wave[w]) {
+      P->items.push_back(items[t].rec);
+      P->dest.push_back(items[t].dest);
+    }
+  }
 
   fiona_plan_stats_t &st = P->st;
   st.n_pmult = n_pm;
@@ -250,20 +335,29 @@ int upload_plan(fiona_plan *P) {
   const fiona_ctx *C = P->ctx;
   const size_t a = 256;
   const size_t o_limbs = 0;
-  const size_t o_outs = align_up(o_limbs + sizeof(LimbConst) * C->L, a);
-  const size_t o_pm = align_up(o_outs + sizeof(uint4) * P->outs.size(), a);
+  const size_t o_items = align_up(o_limbs + sizeof(LimbConst) * C->L, a);
+  const size_t o_dest = align_up(o_items + sizeof(uint4) * P->items.size(), a);
+  const size_t o_waves = align_up(o_dest + sizeof(uint32_t) * P->dest.size(), a);
+  const size_t o_splits = align_up(o_waves + sizeof(uint2) * P->waves.size(), a);
+  const size_t o_pm = align_up(o_splits + sizeof(uint4) * P->splits.size(), a);
   const size_t o_uses = align_up(o_pm + sizeof(uint2) * P->pm.size(), a);
   const size_t o_mats = align_up(o_uses + sizeof(uint4) * P->uses.size(), a);
   const size_t o_mem = align_up(o_mats + sizeof(uint2) * P->mats.size(), a);
-  const size_t total = align_up(o_mem + sizeof(uint2) * P->members.size(), a);
+  const size_t o_sums = align_up(o_mem + sizeof(uint2) * P->members.size(), a);
+  const size_t o_words = align_up(o_sums + sizeof(uint2) * P->sums_dev.size(), a);
+  const size_t total = align_up(o_words + sizeof(uint32_t) * P->members.size() + 4, a);
   std::vector<unsigned char> host(total, 0);
   auto put = [&](size_t off, const void *src, size_t n) { if (n) std::memcpy(host.data() + off, src, n); };
   put(o_limbs, C->limbs.data(), sizeof(LimbConst) * C->L);
-  put(o_outs, P->outs.data(), sizeof(uint4) * P->outs.size());
+  put(o_items, P->items.data(), sizeof(uint4) * P->items.size());
+  put(o_dest, P->dest.data(), sizeof(uint32_t) * P->dest.size());
+  put(o_waves, P->waves.data(), sizeof(uint2) * P->waves.size());
+  put(o_splits, P->splits.data(), sizeof(uint4) * P->splits.size());
   put(o_pm, P->pm.data(), sizeof(uint2) * P->pm.size());
   put(o_uses, P->uses.data(), sizeof(uint4) * P->uses.size());
   put(o_mats, P->mats.data(), sizeof(uint2) * P->mats.size());
   put(o_mem, P->members.data(), sizeof(uint2) * P->members.size());
+  put(o_sums, P->sums_dev.data(), sizeof(uint2) * P->sums_dev.size());
   if (hipGetDevice(&P->device) != hipSuccess) return FIONA_ERR_HIP;
   if (hipMalloc(&P->dev, total) != hipSuccess) {
     P->dev = nullptr;
@@ -272,7 +366,9 @@ int upload_plan(fiona_plan *P) {
   if (hipMemcpy(P->dev, host.data(), total, hipMemcpyHostToDevice) != hipSuccess) return FIONA_ERR_HIP;
   static bool attr_set = false;
   if (!attr_set) {
-    if (hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<kWaves>,
+    if (hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<8>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes) != hipSuccess ||
+        hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<16>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes) != hipSuccess)
       return FIONA_ERR_HIP;
     attr_set = true;
@@ -280,11 +376,16 @@ int upload_plan(fiona_plan *P) {
   unsigned char *base = (unsigned char *)P->dev;
   KParams &k = P->kp;
   k.limbs = (const LimbConst *)(base + o_limbs);
-  k.outs = (const uint4 *)(base + o_outs);
+  k.items = (const uint4 *)(base + o_items);
+  k.dest = (const uint32_t *)(base + o_dest);
+  k.waves = (const uint2 *)(base + o_waves);
+  k.splits = (const uint4 *)(base + o_splits);
   k.pm = (const uint2 *)(base + o_pm);
   k.uses = (const uint4 *)(base + o_uses);
   k.mats = (const uint2 *)(base + o_mats);
   k.members = (const uint2 *)(base + o_mem);
+  k.sums = (const uint2 *)(base + o_sums);
+  k.words = (uint32_t *)(base + o_words);
   return FIONA_OK;
 }
 
@@ -298,7 +399,7 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   if (!ctx || !desc) return FIONA_ERR_ARG;
   int rc = validate_desc(desc);
   if (rc != FIONA_OK) return rc;
-  if (desc->n_in > kMaxInputs) return FIONA_ERR_UNSUPPORTED;
+  if (desc->n_in > FIONA_MAX_INPUTS) return FIONA_ERR_UNSUPPORTED;
   fiona_plan *P = new (std::nothrow) fiona_plan;
   if (!P) return FIONA_ERR_NOMEM;
   P->ctx = ctx;
@@ -318,17 +419,21 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   }
   P->tiles = (ctx->N + fiona::kTile - 1) / fiona::kTile;
   P->grid = P->tiles * ctx->L;
-  P->lds_bytes = (P->n_in + P->n_mat) * kSlotBytes;
+  P->lds_bytes = (P->n_in + P->n_mat + P->n_seg_slots + 1) * kSlotBytes;
   P->st.tile = fiona::kTile;
-  P->st.waves = kWaves;
+  P->st.waves = P->nw;
+  P->st.split_outputs = (uint32_t)P->splits.size();
+  P->st.segment_slots = P->n_seg_slots;
   P->st.lds_bytes = P->lds_bytes;
   P->st.grid = P->grid;
   KParams &k = P->kp;
   k.N = ctx->N;
   k.L = ctx->L;
   k.n_in = P->n_in;
-  k.n_out = P->n_out;
   k.n_mat = P->n_mat;
+  k.n_split = (uint32_t)P->splits.size();
+  k.n_sums = (uint32_t)P->sums_dev.size();
+  k.zero_row = P->n_in + P->n_mat + P->n_seg_slots;
   k.tiles = P->tiles;
   if (!(desc->flags & FIONA_PLAN_HOST_ONLY)) {
     rc = upload_plan(P);
@@ -385,8 +490,14 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   k.signs = ternary_groups;
   k.scales = scales;
   k.out = out_cts;
-  hipLaunchKernelGGL(fiona::hybrid_linear_kernel<kWaves>, dim3(plan->grid), dim3(kWaves * 64),
-                     plan->lds_bytes, stream, k);
+  if (k.n_sums) {   // this call's signs: member words of every distinct sum
+    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((k.n_sums + 3) / 4), dim3(256), 0, stream, k);
+    if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
+  }
+  if (plan->nw == 16)
+    hipLaunchKernelGGL(fiona::hybrid_linear_kernel<16>, dim3(plan->grid), dim3(16 * 64), plan->lds_bytes, stream, k);
+  else
+    hipLaunchKernelGGL(fiona::hybrid_linear_kernel<8>, dim3(plan->grid), dim3(8 * 64), plan->lds_bytes, stream, k);
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   return FIONA_OK;
 }

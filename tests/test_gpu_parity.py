@@ -88,7 +88,7 @@ SMALL = {
     "fold_raw": synth.LayerConfig("fold_raw", N=128, L=2, n_in=8, n_out=3, T=2600, g=8, ternary=0.3),
     "fold_uses": synth.LayerConfig("fold_uses", N=64, L=2, n_in=8, n_out=2, T=4400, g=1, ternary=0.6),
     "big_groups": synth.LayerConfig("big_groups", N=256, L=2, n_in=100, n_out=3, T=400, g=100, ternary=0.5),
-    "lds_full": synth.LayerConfig("lds_full", N=128, L=1, n_in=160, n_out=4, T=320, g=32, ternary=0.5, pool=2),
+    "lds_full": synth.LayerConfig("lds_full", N=128, L=1, n_in=159, n_out=4, T=318, g=53, ternary=0.5, pool=2),
     "all_ternary": synth.LayerConfig("all_ternary", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=1.0, pool=3),
     "all_raw": synth.LayerConfig("all_raw", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=0.0),
 }
