@@ -55,9 +55,9 @@ typedef enum fiona_status {
 /* Limits checked by fiona_ctx_create. */
 #define FIONA_MAX_N (1u << 20)
 #define FIONA_MAX_L 64u
-#define FIONA_MODULUS_BITS 50      /* every modulus satisfies 2 <= q < 2^50 */
+#define FIONA_MODULUS_BITS 50      /* every modulus satisfies 2^20 < q < 2^50 */
 #define FIONA_SCALE_BITS 20        /* every integer scale c satisfies c < 2^20 */
-#define FIONA_MAX_MEMBERS 64u      /* longer ternary groups are split into exact sub-sums */
+#define FIONA_MAX_MEMBERS 48u      /* longer ternary groups are split into exact sub-sums */
 #define FIONA_MAX_INPUTS 159u      /* input ciphertexts per layer: a 64-coefficient tile of every
                                       input (16 B each) plus one zero row fill the 160 KiB LDS */
 
@@ -69,7 +69,8 @@ typedef struct fiona_plan fiona_plan;
  *   N       coefficients per limb, 1 <= N <= FIONA_MAX_N (any N; CKKS uses a
  *           power of two, and the kernel handles a partial last tile);
  *   L       number of RNS limbs, 1 <= L <= FIONA_MAX_L;
- *   moduli  host array of L moduli, each 2 <= q_l < 2^50.  The element-wise
+ *   moduli  host array of L moduli, each 2^20 < q_l < 2^50 (so that every
+ *           integer scale, < 2^20, is a canonical residue).  The element-wise
  *           path does not need them to be NTT-friendly primes; CKKS callers
  *           pass primes q = 1 (mod 2N).
  * Host-only: no device memory is touched.  On success *out owns a context
@@ -129,7 +130,8 @@ typedef struct fiona_layer_desc {
  *     unless FIONA_PLAN_HOST_ONLY.
  * The plan keeps a reference to ctx (which must outlive it).  Errors:
  * FIONA_ERR_ARG, FIONA_ERR_PLAN, FIONA_ERR_UNSUPPORTED (more than FIONA_MAX_INPUTS
- * inputs), FIONA_ERR_NOMEM, FIONA_ERR_HIP.  The plan owns a small device
+ * inputs, or a plaintext table beyond 2^48 bytes), FIONA_ERR_NOMEM, FIONA_ERR_HIP.
+ * The plan owns a small device
  * workspace (the members of its signed sums, reordered by sign on every call),
  * so one plan must not be used by two streams at the same time.
  */

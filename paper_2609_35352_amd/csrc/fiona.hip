@@ -12,7 +12,8 @@
 #include "fiona.h"
 #include "hybrid_kernel.hpp"
 
-using fiona::KParams;
+using fiona::KShape;
+using fiona::PackParams;
 using fiona::LimbConst;
 
 namespace {
@@ -67,12 +68,19 @@ struct fiona_plan {
   uint32_t nw = 8, n_seg_slots = 0;
   std::vector<uint2> pm;
   std::vector<uint4> uses;
-  std::vector<uint2> mats;
+  std::vector<uint32_t> mats;
   std::vector<uint2> members;
   std::vector<uint2> sums_dev;
   void *dev = nullptr;
   int device = -1;
-  KParams kp{};
+  // device pointers into dev
+  const LimbConst *d_limbs = nullptr;
+  const uint4 *d_items = nullptr, *d_splits = nullptr, *d_uses = nullptr;
+  const uint32_t *d_dest = nullptr;
+  const uint2 *d_waves = nullptr, *d_pm = nullptr, *d_members = nullptr, *d_sums = nullptr;
+  const uint32_t *d_mats = nullptr;
+  uint32_t *d_words = nullptr;
+  KShape shape{};
   uint32_t lds_bytes = 0, grid = 0, tiles = 0;
   bool any_signed = false;
 };
@@ -100,7 +108,8 @@ int fiona_ctx_create(uint32_t N, uint32_t L, const uint64_t *moduli, fiona_ctx *
   if (!moduli) return FIONA_ERR_ARG;
   if (N == 0 || N > FIONA_MAX_N || L == 0 || L > FIONA_MAX_L) return FIONA_ERR_UNSUPPORTED;
   for (uint32_t l = 0; l < L; ++l)
-    if (moduli[l] < 2 || moduli[l] >= (1ull << FIONA_MODULUS_BITS)) return FIONA_ERR_UNSUPPORTED;
+    if (moduli[l] <= (1ull << FIONA_SCALE_BITS) || moduli[l] >= (1ull << FIONA_MODULUS_BITS))
+      return FIONA_ERR_UNSUPPORTED;
   fiona_ctx *c = new (std::nothrow) fiona_ctx;
   if (!c) return FIONA_ERR_NOMEM;
   try {
@@ -159,6 +168,7 @@ struct SumBuild {
   uint32_t n_use = 0;
   uint32_t slot = fiona::kInlineSum;
   uint32_t mem_begin = 0;
+  uint32_t word_begin = 0;   // header word, then the member words
 };
 
 int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
@@ -256,13 +266,14 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   uint64_t addsub_shared = 0;
   for (auto &sb : sums) {
     sb.mem_begin = (uint32_t)P->members.size();
+    sb.word_begin = (uint32_t)P->sums_dev.size() * fiona::kSumWords;
     for (auto &m : sb.members) P->members.push_back(m);
     P->sums_dev.push_back(make_uint2(sb.mem_begin, (uint32_t)sb.members.size()));
     addsub_shared += sb.members.size() - 1;
   }
   for (uint32_t s : cand) {
     sums[s].slot = (uint32_t)P->mats.size();
-    P->mats.push_back(make_uint2(sums[s].mem_begin, (uint32_t)sums[s].members.size()));
+    P->mats.push_back(sums[s].word_begin);
   }
   P->n_mat = (uint32_t)P->mats.size();
   std::vector<uint32_t> use_begin(d->n_out);
@@ -270,11 +281,15 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
     use_begin[j] = (uint32_t)P->uses.size();
     for (const Use &u : out_uses[j]) {
       const SumBuild &sb = sums[u.sum];
-      P->uses.push_back(make_uint4(sb.mem_begin, (uint32_t)sb.members.size(), sb.slot,
-                                   u.scale | (u.neg ? 0x80000000u : 0u)));
+      P->uses.push_back(make_uint4(sb.word_begin, sb.slot, u.scale | (u.neg ? 0x80000000u : 0u), 0));
     }
   }
-  for (uint32_t t = 0; t < n_pm; ++t) P->pm.push_back(make_uint2(d->pm_pt[t], d->pm_input[t]));
+  // raw-term records: byte offset of the plaintext row (48 bits) and the input
+  const uint64_t ln8 = (uint64_t)P->ctx->L * P->ctx->N * 8;
+  for (uint32_t t = 0; t < n_pm; ++t) {
+    const uint64_t off = (uint64_t)d->pm_pt[t] * ln8;
+    P->pm.push_back(make_uint2((uint32_t)off, (uint32_t)(off >> 32) | (d->pm_input[t] << 16)));
+  }
 
   // items, each with its cost; segments of a split output get consecutive LDS slots
   struct Item { uint4 rec; uint32_t dest; double cost; };
@@ -342,10 +357,11 @@ int upload_plan(fiona_plan *P) {
   const size_t o_pm = align_up(o_splits + sizeof(uint4) * P->splits.size(), a);
   const size_t o_uses = align_up(o_pm + sizeof(uint2) * P->pm.size(), a);
   const size_t o_mats = align_up(o_uses + sizeof(uint4) * P->uses.size(), a);
-  const size_t o_mem = align_up(o_mats + sizeof(uint2) * P->mats.size(), a);
+  const size_t o_mem = align_up(o_mats + sizeof(uint32_t) * P->mats.size(), a);
   const size_t o_sums = align_up(o_mem + sizeof(uint2) * P->members.size(), a);
   const size_t o_words = align_up(o_sums + sizeof(uint2) * P->sums_dev.size(), a);
-  const size_t total = align_up(o_words + sizeof(uint32_t) * P->members.size() + 4, a);
+  const size_t n_words = P->sums_dev.size() * fiona::kSumWords;
+  const size_t total = align_up(o_words + sizeof(uint32_t) * n_words, a);
   std::vector<unsigned char> host(total, 0);
   auto put = [&](size_t off, const void *src, size_t n) { if (n) std::memcpy(host.data() + off, src, n); };
   put(o_limbs, C->limbs.data(), sizeof(LimbConst) * C->L);
@@ -355,7 +371,7 @@ int upload_plan(fiona_plan *P) {
   put(o_splits, P->splits.data(), sizeof(uint4) * P->splits.size());
   put(o_pm, P->pm.data(), sizeof(uint2) * P->pm.size());
   put(o_uses, P->uses.data(), sizeof(uint4) * P->uses.size());
-  put(o_mats, P->mats.data(), sizeof(uint2) * P->mats.size());
+  put(o_mats, P->mats.data(), sizeof(uint32_t) * P->mats.size());
   put(o_mem, P->members.data(), sizeof(uint2) * P->members.size());
   put(o_sums, P->sums_dev.data(), sizeof(uint2) * P->sums_dev.size());
   if (hipGetDevice(&P->device) != hipSuccess) return FIONA_ERR_HIP;
@@ -374,18 +390,17 @@ int upload_plan(fiona_plan *P) {
     attr_set = true;
   }
   unsigned char *base = (unsigned char *)P->dev;
-  KParams &k = P->kp;
-  k.limbs = (const LimbConst *)(base + o_limbs);
-  k.items = (const uint4 *)(base + o_items);
-  k.dest = (const uint32_t *)(base + o_dest);
-  k.waves = (const uint2 *)(base + o_waves);
-  k.splits = (const uint4 *)(base + o_splits);
-  k.pm = (const uint2 *)(base + o_pm);
-  k.uses = (const uint4 *)(base + o_uses);
-  k.mats = (const uint2 *)(base + o_mats);
-  k.members = (const uint2 *)(base + o_mem);
-  k.sums = (const uint2 *)(base + o_sums);
-  k.words = (uint32_t *)(base + o_words);
+  P->d_limbs = (const LimbConst *)(base + o_limbs);
+  P->d_items = (const uint4 *)(base + o_items);
+  P->d_dest = (const uint32_t *)(base + o_dest);
+  P->d_waves = (const uint2 *)(base + o_waves);
+  P->d_splits = (const uint4 *)(base + o_splits);
+  P->d_pm = (const uint2 *)(base + o_pm);
+  P->d_uses = (const uint4 *)(base + o_uses);
+  P->d_mats = (const uint32_t *)(base + o_mats);
+  P->d_members = (const uint2 *)(base + o_mem);
+  P->d_sums = (const uint2 *)(base + o_sums);
+  P->d_words = (uint32_t *)(base + o_words);
   return FIONA_OK;
 }
 
@@ -400,6 +415,8 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   int rc = validate_desc(desc);
   if (rc != FIONA_OK) return rc;
   if (desc->n_in > FIONA_MAX_INPUTS) return FIONA_ERR_UNSUPPORTED;
+  // raw-term records hold 48-bit byte offsets into the plaintext table
+  if ((uint64_t)desc->n_pt * ctx->L * ctx->N * 8 > (1ull << 48)) return FIONA_ERR_UNSUPPORTED;
   fiona_plan *P = new (std::nothrow) fiona_plan;
   if (!P) return FIONA_ERR_NOMEM;
   P->ctx = ctx;
@@ -426,13 +443,12 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   P->st.segment_slots = P->n_seg_slots;
   P->st.lds_bytes = P->lds_bytes;
   P->st.grid = P->grid;
-  KParams &k = P->kp;
+  KShape &k = P->shape;
   k.N = ctx->N;
   k.L = ctx->L;
   k.n_in = P->n_in;
   k.n_mat = P->n_mat;
   k.n_split = (uint32_t)P->splits.size();
-  k.n_sums = (uint32_t)P->sums_dev.size();
   k.zero_row = P->n_in + P->n_mat + P->n_seg_slots;
   k.tiles = P->tiles;
   if (!(desc->flags & FIONA_PLAN_HOST_ONLY)) {
@@ -484,20 +500,22 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   if (plan->n_out == 0) return FIONA_OK;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return FIONA_ERR_ARG;
-  KParams k = plan->kp;
-  k.in = in_cts;
-  k.pt = pt_diags;
-  k.signs = ternary_groups;
-  k.scales = scales;
-  k.out = out_cts;
-  if (k.n_sums) {   // this call's signs: member words of every distinct sum
-    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((k.n_sums + 3) / 4), dim3(256), 0, stream, k);
+  const uint32_t n_sums = (uint32_t)plan->sums_dev.size();
+  if (n_sums) {   // this call's signs: the words of every distinct sum
+    PackParams pp;
+    pp.signs = ternary_groups;
+    pp.members = plan->d_members;
+    pp.sums = plan->d_sums;
+    pp.words = plan->d_words;
+    pp.n_sums = n_sums;
+    pp.zero_row = plan->shape.zero_row;
+    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((n_sums + 3) / 4), dim3(256), 0, stream, pp);
     if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   }
-  if (plan->nw == 16)
-    hipLaunchKernelGGL(fiona::hybrid_linear_kernel<16>, dim3(plan->grid), dim3(16 * 64), plan->lds_bytes, stream, k);
-  else
-    hipLaunchKernelGGL(fiona::hybrid_linear_kernel<8>, dim3(plan->grid), dim3(8 * 64), plan->lds_bytes, stream, k);
+  auto kernel = plan->nw == 16 ? fiona::hybrid_linear_kernel<16> : fiona::hybrid_linear_kernel<8>;
+  hipLaunchKernelGGL(kernel, dim3(plan->grid), dim3(plan->nw * 64), plan->lds_bytes, stream, in_cts, pt_diags,
+                     scales, out_cts, plan->d_limbs, plan->d_items, plan->d_dest, plan->d_waves, plan->d_splits,
+                     plan->d_pm, plan->d_uses, plan->d_mats, plan->d_words, plan->shape);
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   return FIONA_OK;
 }

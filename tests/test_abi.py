@@ -159,9 +159,9 @@ def test_long_groups_are_split_and_zero_groups_dropped():
                 grp_off=[0, 1, 2], grp_mem_off=[0, n, n + 4], mem_input=list(range(n)) + [0, 1, 2, 3],
                 mem_sign=[1] * n + [0, 0, 0, 0], grp_scale=[0, 1])
     st = fiona.Plan(ctx, flags=HOST, **args).stats()
-    assert st["n_use"] == 3            # ceil(150 / 64) sub-sums; the all-zero group contributes nothing
+    assert st["n_use"] == 4            # ceil(150 / 48) sub-sums; the all-zero group contributes nothing
     assert st["n_member_nonzero"] == 150 and st["n_member"] == 154
-    assert st["pmult_grouped"] == 3 and st["pmult_per_contribution"] == 150
+    assert st["pmult_grouped"] == 4 and st["pmult_per_contribution"] == 150
 
 
 @pytest.mark.parametrize("name", ["vgg11", "vit768", "bert_ffn"])

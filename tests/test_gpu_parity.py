@@ -300,3 +300,21 @@ def test_full_size_all_pmult_route_equivalence(dev):
     _check_sampled(allpm, out_a, in_t, 16, 102, "vgg11 all-PMult")
     del out_h, out_a, in_t
     torch.cuda.empty_cache()
+
+
+def test_runtime_signs_are_read(dev):
+    """The kernel takes the member signs from ternary_groups on every call: with
+    a plan built without sharing, flipping or zeroing members' signs after plan
+    creation gives the oracle's result for the new signs."""
+    layer = _small_layer("ragged_pool")
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    rng = np.random.default_rng(3)
+    signs2 = layer.mem_sign.copy()
+    nz = np.nonzero(signs2)[0]
+    pick = rng.choice(nz, size=len(nz) // 3, replace=False)
+    signs2[pick[: len(pick) // 2]] *= -1
+    signs2[pick[len(pick) // 2:]] = 0
+    lay2 = synth.Layer(**{**layer.__dict__, "mem_sign": signs2})
+    expect = oracle.weighted_sum_layer(lay2, x, pt)
+    out_t, *_ = _run(layer, dev, x, pt, flags=fiona.FIONA_PLAN_NO_SHARING, signs=signs2)
+    _assert_equal(_host(out_t, layer), expect, "run-time signs")
