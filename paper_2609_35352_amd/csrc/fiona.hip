@@ -28,13 +28,16 @@ constexpr double kCostUseResident = 0.6;
 constexpr double kCostUseInline = 0.5;
 constexpr double kCostMember = 0.25;
 constexpr double kCostFinish = 6.0;
+constexpr double kCostChunk = 3.0;
 constexpr double kMinSegmentCost = 128.0;
 
 LimbConst make_limb_const(uint64_t q) {
   LimbConst c;
   c.q = q;
-  c.r50 = (uint64_t)((((unsigned __int128)1) << 50) % q);
-  c.r50_shoup = (uint64_t)((((unsigned __int128)c.r50) << 64) / q);
+  c.r32 = (uint64_t)((((unsigned __int128)1) << 32) % q);
+  c.r32_shoup = (uint64_t)((((unsigned __int128)c.r32) << 64) / q);
+  c.r57 = (uint64_t)((((unsigned __int128)1) << 57) % q);
+  c.r57_shoup = (uint64_t)((((unsigned __int128)c.r57) << 64) / q);
   c.qinv = 1.0 / (double)q;
   return c;
 }
@@ -284,28 +287,55 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
       P->uses.push_back(make_uint4(sb.word_begin, sb.slot, u.scale | (u.neg ? 0x80000000u : 0u), 0));
     }
   }
-  // raw-term records: byte offset of the plaintext row (48 bits) and the input
+  // Raw-term records, per work item, in chunks of at most kChunkTerms terms
+  // (one block of kChunkSlots records each, see hybrid_kernel.hpp).  The
+  // terms of an output may be taken in any order (the sum is exact), so they
+  // are sorted by plaintext offset: a chunk then covers a short stretch of the
+  // plaintext table, and its terms' offsets from the chunk base fit 31 bits.
+  const uint32_t zero_row = d->n_in + (uint32_t)P->mats.size() + seg_slots;
   const uint64_t ln8 = (uint64_t)P->ctx->L * P->ctx->N * 8;
-  for (uint32_t t = 0; t < n_pm; ++t) {
-    const uint64_t off = (uint64_t)d->pm_pt[t] * ln8;
-    P->pm.push_back(make_uint2((uint32_t)off, (uint32_t)(off >> 32) | (d->pm_input[t] << 16)));
-  }
+  auto emit_chunks = [&](const std::vector<std::pair<uint64_t, uint32_t>> &terms, size_t t0, size_t t1) {
+    const uint32_t first = (uint32_t)(P->pm.size() / fiona::kChunkSlots);
+    size_t t = t0;
+    while (t < t1) {
+      const uint64_t cbase = terms[t].first;
+      size_t e = t;
+      while (e < t1 && e - t < fiona::kChunkTerms && terms[e].first - cbase < (1ull << 31)) ++e;
+      const uint32_t n = (uint32_t)(e - t), nb = (n + fiona::kRawBatch - 1) / fiona::kRawBatch;
+      const size_t blk = P->pm.size();
+      P->pm.resize(blk + fiona::kChunkSlots, make_uint2(0, 0));
+      for (uint32_t r = 0; r < nb * fiona::kRawBatch; ++r)
+        P->pm[blk + r] = r < n ? make_uint2((uint32_t)(terms[t + r].first - cbase), terms[t + r].second * kSlotBytes)
+                               : make_uint2(0, zero_row * kSlotBytes);
+      P->pm[blk + fiona::kChunkSlots - 1] = make_uint2((uint32_t)cbase, (uint32_t)(cbase >> 32) | (nb << 16));
+      t = e;
+    }
+    return make_uint2(first, (uint32_t)(P->pm.size() / fiona::kChunkSlots) - first);
+  };
 
   // items, each with its cost; segments of a split output get consecutive LDS slots
   struct Item { uint4 rec; uint32_t dest; double cost; };
   std::vector<Item> items;
   uint32_t slot = 0;
+  std::vector<std::pair<uint64_t, uint32_t>> terms;   // (plaintext byte offset, input)
   for (uint32_t j = 0; j < d->n_out; ++j) {
     const uint32_t pb = d->pm_off[j], pc = d->pm_off[j + 1] - pb;
+    terms.clear();
+    for (uint32_t t = pb; t < pb + pc; ++t) terms.push_back({(uint64_t)d->pm_pt[t] * ln8, d->pm_input[t]});
+    std::stable_sort(terms.begin(), terms.end(),
+                     [](const std::pair<uint64_t, uint32_t> &a, const std::pair<uint64_t, uint32_t> &b) {
+                       return a.first < b.first;
+                     });
     const uint32_t ub = use_begin[j], uc = (uint32_t)out_uses[j].size();
     const uint32_t S = nseg[j];
     if (S > 1) P->splits.push_back(make_uint4(j, slot, S, 0));
     for (uint32_t g = 0; g < S; ++g) {
       const uint32_t r0 = (uint32_t)((uint64_t)pc * g / S), r1 = (uint32_t)((uint64_t)pc * (g + 1) / S);
       const uint32_t u0 = (uint32_t)((uint64_t)uc * g / S), u1 = (uint32_t)((uint64_t)uc * (g + 1) / S);
-      double c = kCostFinish + (double)(r1 - r0);
+      const uint2 ch = emit_chunks(terms, r0, r1);
+      double c = kCostFinish + (double)(r1 - r0) + kCostChunk * ch.y;
       for (uint32_t u = u0; u < u1; ++u) c += use_cost(out_uses[j][u]);
-      items.push_back(Item{make_uint4(pb + r0, r1 - r0, ub + u0, u1 - u0),
+      items.push_back(Item{make_uint4(ch.x, ch.y, ub + u0, u1 - u0),
                            S > 1 ? (fiona::kSegmentFlag | (slot + g)) : j, c});
     }
     if (S > 1) slot += S;

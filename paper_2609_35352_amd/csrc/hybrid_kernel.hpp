@@ -33,9 +33,18 @@ constexpr uint32_t kTile = 64;            // coefficients per workgroup (one per
 constexpr uint32_t kRowBytes = kTile * 16;   // one LDS row: 16 B per lane
 constexpr uint32_t kInlineSum = 0xFFFFFFFFu;
 constexpr uint32_t kRawBatch = 8;         // plaintext loads per batch; two batches in flight
+constexpr uint32_t kRawBatches = kChunkTerms / kRawBatch;   // batches per chunk of raw records
+constexpr uint32_t kChunkSlots = 64;      // records per chunk block; the last one is the header
 constexpr uint32_t kSumBatch = 8;         // member reads issued before their additions
+constexpr uint32_t kSumBatches = kMaxMembers / kSumBatch;
 constexpr uint32_t kSumWords = 64;        // words per distinct sum: header + padded member rows
 constexpr uint32_t kSegmentFlag = 0x80000000u;
+constexpr int kLoadNT = 2;                // cache policy of the plaintext stream: nontemporal
+static_assert(kChunkTerms % kRawBatch == 0 && kChunkTerms < kChunkSlots, "chunk layout");
+// header, rows to add from word 1 up, rows to subtract from word 62 down, each list padded to a batch
+static_assert(1 + kMaxMembers + 2 * (kSumBatch - 1) <= kSumWords - 1, "sum block layout");
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Per-call description for the sign-packing kernel.
 struct PackParams {
@@ -55,12 +64,12 @@ __device__ __forceinline__ uint64_t pair64(uint32_t lo, uint32_t hi) { return ((
 __device__ __forceinline__ uint32_t pad8(uint32_t n) { return (n + 7u) & ~7u; }
 __device__ __forceinline__ uint32_t bcast(uint32_t v, uint32_t l) { return __builtin_amdgcn_readlane(v, l); }
 
-// The words of every distinct signed sum for this call.  Word 0 counts the
-// members to add and to subtract, each rounded up to a batch of 8; then come
-// the LDS byte offsets of the members' rows, added ones first, then the
-// subtracted ones, each list padded with the all-zero row.  Members whose
-// run-time sign is 0 are left out (Sec. 3 Obs. 2, the skip).  One wavefront
-// per sum.
+// The words of every distinct signed sum for this call.  Word 0 holds the
+// numbers of rows to add and to subtract, each rounded up to a batch of 8;
+// the rows to add follow from word 1 upwards and the rows to subtract from
+// word 62 downwards, each list padded with the all-zero row.  A row is given
+// as its LDS byte offset.  Members whose run-time sign is 0 are left out
+// (Sec. 3 Obs. 2, the skip).  One wavefront per sum.
 __global__ void __launch_bounds__(256) pack_members_kernel(const PackParams P) {
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t s = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -78,14 +87,38 @@ __global__ void __launch_bounds__(256) pack_members_kernel(const PackParams P) {
   const uint32_t n0 = __popcll(b0), n1 = __popcll(b1), p0 = pad8(n0), p1 = pad8(n1);
   uint32_t *w = P.words + (size_t)s * kSumWords;
   if (cls == 0) w[1 + __popcll(b0 & below)] = row * kRowBytes;
-  if (cls == 1) w[1 + p0 + __popcll(b1 & below)] = row * kRowBytes;
+  if (cls == 1) w[62 - __popcll(b1 & below)] = row * kRowBytes;
   const uint32_t zero = P.zero_row * kRowBytes;
-  if ((lane >= n0 && lane < p0) || (lane >= p0 + n1 && lane < p0 + p1)) w[1 + lane] = zero;
+  if (lane >= 1 + n0 && lane < 1 + p0) w[lane] = zero;
+  if (lane + n1 <= 62 && lane + p1 > 62) w[lane] = zero;
   if (lane == 0) w[0] = p0 | (p1 << 16);
 }
 
 __device__ __forceinline__ const uint4 &lds_row(const uint4 *lds, uint32_t row_bytes, uint32_t lane_bytes) {
   return *(const uint4 *)((const char *)lds + row_bytes + lane_bytes);
+}
+
+// Adds the rows at word lanes first + step * u (u = 0..7) into the packed digit sums.
+template <int First, int Step>
+__device__ __forceinline__ void sum_batch(uint64_t &a, uint64_t &b, uint32_t wv, const uint4 *lds, uint32_t lane16) {
+  uint4 x[kSumBatch];
+#pragma unroll
+  for (int u = 0; u < (int)kSumBatch; ++u) x[u] = lds_row(lds, bcast(wv, First + Step * u), lane16);
+#pragma unroll
+  for (int u = 0; u < (int)kSumBatch; ++u) {
+    a += pair64(x[u].x, x[u].y);
+    b += pair64(x[u].z, x[u].w);
+  }
+}
+
+template <int K>
+__device__ __forceinline__ void sum_rows(uint32_t np, uint32_t nn, uint64_t &pa, uint64_t &pb, uint64_t &na,
+                                         uint64_t &nb, uint32_t wv, const uint4 *lds, uint32_t lane16) {
+  if constexpr (K < (int)kSumBatches) {
+    if (K * kSumBatch < np) sum_batch<1 + K * kSumBatch, 1>(pa, pb, wv, lds, lane16);
+    if (K * kSumBatch < nn) sum_batch<62 - K * kSumBatch, -1>(na, nb, wv, lds, lane16);
+    sum_rows<K + 1>(np, nn, pa, pb, na, nb, wv, lds, lane16);
+  }
 }
 
 // Signed sum U = sum h x of one distinct sum whose words are in wv (one per
@@ -94,58 +127,68 @@ __device__ __forceinline__ const uint4 &lds_row(const uint4 *lds, uint32_t row_b
 // other for at most 48 members), in batches of 8 LDS reads.
 __device__ __forceinline__ uint4 signed_sum(uint32_t wv, const uint4 *lds, uint32_t lane16) {
   const uint32_t hdr = bcast(wv, 0);
-  const uint32_t np = hdr & 0xFFFFu, nn = hdr >> 16;
   uint64_t pa = 0, pb = 0, na = 0, nb = 0;
-  for (uint32_t r = 0; r < np; r += kSumBatch) {
-    uint4 x[kSumBatch];
-#pragma unroll
-    for (uint32_t u = 0; u < kSumBatch; ++u) x[u] = lds_row(lds, bcast(wv, 1 + r + u), lane16);
-#pragma unroll
-    for (uint32_t u = 0; u < kSumBatch; ++u) {
-      pa += pair64(x[u].x, x[u].y);
-      pb += pair64(x[u].z, x[u].w);
-    }
-  }
-  for (uint32_t r = 0; r < nn; r += kSumBatch) {
-    uint4 x[kSumBatch];
-#pragma unroll
-    for (uint32_t u = 0; u < kSumBatch; ++u) x[u] = lds_row(lds, bcast(wv, 1 + np + r + u), lane16);
-#pragma unroll
-    for (uint32_t u = 0; u < kSumBatch; ++u) {
-      na += pair64(x[u].x, x[u].y);
-      nb += pair64(x[u].z, x[u].w);
-    }
-  }
+  sum_rows<0>(hdr & 0xFFFFu, hdr >> 16, pa, pb, na, nb, wv, lds, lane16);
   return make_uint4((uint32_t)pa - (uint32_t)na, (uint32_t)(pa >> 32) - (uint32_t)(na >> 32),
                     (uint32_t)pb - (uint32_t)nb, (uint32_t)(pb >> 32) - (uint32_t)(nb >> 32));
 }
 
-// A raw-term record (one per lane): byte offset of the term's plaintext
-// (low 32 bits; bits 32..47 in the low half of .y) and its input (high half of .y).
-__device__ __forceinline__ uint64_t pt_offset(uint2 rec, uint32_t r) {
-  return pair64(bcast(rec.x, r), bcast(rec.y, r) & 0xFFFFu);
+// Raw-term chunks.  A chunk is a block of kChunkSlots records (one per lane):
+// record r < 8 nb is {byte offset of the term's plaintext from the chunk
+// base, LDS byte offset of the term's input row}; padding records point at
+// offset 0 and the all-zero row, so they add nothing.  The header record (the
+// last lane) is {chunk base bits 0..31, bits 32..47 | nb << 16}; the chunk
+// base is a byte offset into the plaintext table.  The plaintext of record r
+// is read with a buffer load: descriptor base = this tile's plaintext column
+// at the chunk base, lane offset in a VGPR, record offset in an SGPR.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const char *pt_tile, uint2 rec, uint32_t &nb) {
+  const uint32_t lo = bcast(rec.x, kChunkSlots - 1), hi = bcast(rec.y, kChunkSlots - 1);
+  nb = hi >> 16;
+  const char *base = pt_tile + pair64(lo, hi & 0xFFFFu);
+  return __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)0xFFFFFFFF, 0x00020000);
 }
-__device__ __forceinline__ uint32_t in_row(uint2 rec, uint32_t r) { return (bcast(rec.y, r) >> 16) * kRowBytes; }
 
-// Issue the plaintext loads of 8 raw terms (records r0 .. r0+7 of the chunk).
-__device__ __forceinline__ void raw_issue(uint64_t (&w)[kRawBatch], uint2 rec, uint32_t r0,
-                                          const uint64_t *pt_lane) {
+// Issue the plaintext loads of the batch of records r0 .. r0+7 of a chunk.
+__device__ __forceinline__ void raw_issue(u32x2 (&w)[kRawBatch], __amdgpu_buffer_rsrc_t rs, uint2 rec, uint32_t r0,
+                                          uint32_t voff) {
 #pragma unroll
   for (uint32_t u = 0; u < kRawBatch; ++u)
-    w[u] = __builtin_nontemporal_load((const uint64_t *)((const char *)pt_lane + pt_offset(rec, r0 + u)));
+    w[u] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, bcast(rec.x, r0 + u), kLoadNT);
 }
 
-// Multiply-accumulate 8 raw terms whose plaintext words are in w.
-__device__ __forceinline__ void raw_consume(Acc &a0, Acc &a1, const uint64_t (&w)[kRawBatch], uint2 rec,
-                                            uint32_t r0, const uint4 *lds, uint32_t lane16) {
+// Multiply-accumulate the batch of records r0 .. r0+7, whose plaintext words are in w.
+__device__ __forceinline__ void raw_consume(Acc &a0, Acc &a1, const u32x2 (&w)[kRawBatch], uint2 rec, uint32_t r0,
+                                            const uint4 *lds, uint32_t lane16) {
   uint4 x[kRawBatch];
 #pragma unroll
-  for (uint32_t u = 0; u < kRawBatch; ++u) x[u] = lds_row(lds, in_row(rec, r0 + u), lane16);
+  for (uint32_t u = 0; u < kRawBatch; ++u) x[u] = lds_row(lds, bcast(rec.y, r0 + u), lane16);
 #pragma unroll
   for (uint32_t u = 0; u < kRawBatch; ++u) {
-    const uint32_t w0 = lo_digit(w[u]), w1 = hi_digit(w[u]);
-    mac(a0, x[u].x, x[u].y, w0, w1);
-    mac(a1, x[u].z, x[u].w, w0, w1);
+    mac(a0, x[u].x, x[u].y, w[u].x, w[u].y);
+    mac(a1, x[u].z, x[u].w, w[u].x, w[u].y);
+  }
+}
+
+// All nb batches of a chunk: a software pipeline that keeps batch b+1 in
+// flight while batch b is multiplied.  The steady state issues the same
+// loads on every path, so the wait counts stay exact.
+__device__ __forceinline__ void raw_chunk(uint32_t nb, __amdgpu_buffer_rsrc_t rs, uint2 rec, uint32_t voff, Acc &a0,
+                                          Acc &a1, const uint4 *lds, uint32_t lane16) {
+  u32x2 wa[kRawBatch], wb[kRawBatch];
+  raw_issue(wa, rs, rec, 0, voff);
+  uint32_t b = 0;
+  for (; b + 2 < nb; b += 2) {   // batch b is in flight in wa
+    raw_issue(wb, rs, rec, (b + 1) * kRawBatch, voff);
+    raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
+    raw_issue(wa, rs, rec, (b + 2) * kRawBatch, voff);
+    raw_consume(a0, a1, wb, rec, (b + 1) * kRawBatch, lds, lane16);
+  }
+  if (b + 1 < nb) {   // two batches left, the first in flight in wa
+    raw_issue(wb, rs, rec, (b + 1) * kRawBatch, voff);
+    raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
+    raw_consume(a0, a1, wb, rec, (b + 1) * kRawBatch, lds, lane16);
+  } else {
+    raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
   }
 }
 
@@ -156,8 +199,8 @@ __device__ __forceinline__ void fold(Acc &a0, Acc &a1, uint64_t &r0, uint64_t &r
   acc_zero(a1);
 }
 
-__device__ __forceinline__ uint2 load_raw_chunk(const uint2 *pm, uint32_t begin, uint32_t count, uint32_t lane) {
-  return lane < count ? pm[begin + lane] : make_uint2(0, 0);
+__device__ __forceinline__ uint2 load_chunk(const uint2 *pm, uint32_t chunk, uint32_t lane) {
+  return pm[(size_t)chunk * kChunkSlots + lane];
 }
 __device__ __forceinline__ uint4 load_use_chunk(const uint4 *uses, uint32_t begin, uint32_t count, uint32_t lane) {
   return lane < count ? uses[begin + lane] : make_uint4(0, kInlineSum, 0, 0);
@@ -190,7 +233,7 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
     const uint64_t b = __builtin_nontemporal_load(src + LN + lane_off);
     lds[i * kTile + lane] = make_uint4(lo_digit(a), hi_digit(a), lo_digit(b), hi_digit(b));
   }
-  if (wave == NW - 1) lds[S.zero_row * kTile + lane] = make_uint4(0, 0, 0, 0);   // padding row of sums
+  if (wave == NW - 1) lds[S.zero_row * kTile + lane] = make_uint4(0, 0, 0, 0);   // padding row
   __syncthreads();
 
   // 2. shared signed sums, formed once per tile
@@ -199,21 +242,22 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
     sums[s * kTile + lane] = signed_sum(words[(size_t)mats[s] + lane], lds, lane16);
   __syncthreads();
 
-  // 3. this wavefront's work items; the first chunks of records of each item
-  // are loaded while the previous item runs
+  // 3. this wavefront's work items; the first records of each item are loaded
+  // while the previous item runs
   uint4 *segs = sums + (size_t)S.n_mat * kTile;
-  const uint64_t *pt_lane = pt + (size_t)limb * S.N + k0 + lane_off;
+  const char *pt_tile = (const char *)(pt + (size_t)limb * S.N + k0);
+  const uint32_t voff = lane_off * 8u;
   const uint2 wr = waves[wave];
   uint4 item_next = wr.y ? items[wr.x] : make_uint4(0, 0, 0, 0);
-  uint2 raw_next = load_raw_chunk(pm, item_next.x, min(64u, item_next.y), lane);
+  uint2 raw_next = item_next.y ? load_chunk(pm, item_next.x, lane) : make_uint2(0, 0);
   uint4 use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
   for (uint32_t it = wr.x; it < wr.x + wr.y; ++it) {
-    const uint4 item = item_next;
+    const uint4 item = item_next;   // first chunk, chunks, first use, uses
     uint2 raw_rec = raw_next;
     uint4 use_rec = use_next;
     if (it + 1 < wr.x + wr.y) {
       item_next = items[it + 1];
-      raw_next = load_raw_chunk(pm, item_next.x, min(64u, item_next.y), lane);
+      raw_next = item_next.y ? load_chunk(pm, item_next.x, lane) : make_uint2(0, 0);
       use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
     }
     // member words of this item's first in-place sum
@@ -224,41 +268,18 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
     acc_zero(a1);
     uint64_t r0 = 0, r1 = 0;
 
-    // raw route: one PMult per term, in chunks of 64 records; within a chunk a
-    // software pipeline over batches of 8 keeps batch b+1 in flight while
-    // batch b is multiplied (the steady state issues the same loads on every
-    // path, so the wait counts stay exact)
-    for (uint32_t base = 0; base < item.y; base += 64) {
-      const uint32_t n = min(64u, item.y - base);
+    // raw route: one PMult per term, chunk by chunk; within a chunk batch b+1
+    // is in flight while batch b is multiplied
+    for (uint32_t c = 0; c < item.y; ++c) {
       const uint2 rec = raw_rec;
-      if (base + 64 < item.y) raw_rec = load_raw_chunk(pm, item.x + base + 64, min(64u, item.y - base - 64), lane);
-      if (base && base % kFoldTerms == 0) fold(a0, a1, r0, r1, lc);   // keep the accumulators exact
-      const uint32_t nb = n / kRawBatch;
-      uint64_t wa[kRawBatch], wb[kRawBatch];
-      if (nb) {
-        raw_issue(wa, rec, 0, pt_lane);
-        uint32_t b = 0;
-        for (; b + 2 < nb; b += 2) {   // batch b is in flight in wa
-          raw_issue(wb, rec, (b + 1) * kRawBatch, pt_lane);
-          raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
-          raw_issue(wa, rec, (b + 2) * kRawBatch, pt_lane);
-          raw_consume(a0, a1, wb, rec, (b + 1) * kRawBatch, lds, lane16);
-        }
-        if (b + 1 < nb) {   // two batches left, the first in flight in wa
-          raw_issue(wb, rec, (b + 1) * kRawBatch, pt_lane);
-          raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
-          raw_consume(a0, a1, wb, rec, (b + 1) * kRawBatch, lds, lane16);
-        } else {
-          raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
-        }
+      if (c + 1 < item.y) raw_rec = load_chunk(pm, item.x + c + 1, lane);
+      if (c) {
+        if (c % kFoldChunks == 0) fold(a0, a1, r0, r1, lc);   // keep the accumulators exact
+        else { carry(a0); carry(a1); }
       }
-      for (uint32_t r = nb * kRawBatch; r < n; ++r) {
-        const uint64_t w = __builtin_nontemporal_load((const uint64_t *)((const char *)pt_lane + pt_offset(rec, r)));
-        const uint4 x = lds_row(lds, in_row(rec, r), lane16);
-        const uint32_t w0 = lo_digit(w), w1 = hi_digit(w);
-        mac(a0, x.x, x.y, w0, w1);
-        mac(a1, x.z, x.w, w0, w1);
-      }
+      uint32_t nb;
+      const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(pt_tile, rec, nb);
+      raw_chunk(nb, rs, rec, voff, a0, a1, lds, lane16);
     }
 
     // signed route: each use applies its group's scale once to a signed sum;
@@ -268,7 +289,7 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
       const uint4 rec = use_rec;   // word begin, LDS slot or kInlineSum, scale | negate << 31, 0
       if (base + 64 < item.w) use_rec = load_use_chunk(uses, item.z + base + 64, min(64u, item.w - base - 64), lane);
       const uint32_t scl = lane < n ? (uint32_t)scales[rec.z & 0x7FFFFFFFu] : 0u;   // scales are < 2^20
-      if (base && base % kFoldTerms == 0) fold(a0, a1, r0, r1, lc);
+      if (base && base % kFoldUses == 0) fold(a0, a1, r0, r1, lc);
       for (uint32_t r = 0; r < n; ++r) {
         const uint32_t slot = bcast(rec.y, r);
         const uint32_t wcur = words_next;
