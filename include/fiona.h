@@ -83,6 +83,7 @@ void fiona_ctx_destroy(fiona_ctx *ctx);
 #define FIONA_PLAN_NO_SHARING 1u   /* evaluate every group's signed sum on its own (no reuse) */
 #define FIONA_PLAN_HOST_ONLY 2u    /* build and check the plan on the host; upload nothing */
 #define FIONA_PLAN_NO_LDS_SUMS 4u  /* never keep shared signed sums resident in LDS */
+#define FIONA_PLAN_NO_PARTIAL_SHARING 8u   /* share only whole signed sums, no common sub-sums */
 
 /*
  * One routed layer, in the raw per-(output, term) form the offline compiler
@@ -126,6 +127,15 @@ typedef struct fiona_layer_desc {
  *     exactly opposite (same inputs, same or all reversed signs) across the
  *     layer and computes each once (Sec. 4.2 "Sharing Signed Sums"); sums
  *     used more than once are kept resident in LDS per position tile;
+ *   - unless FIONA_PLAN_NO_SHARING or FIONA_PLAN_NO_PARTIAL_SHARING, also
+ *     shares signed terms common to several sums that only partly overlap
+ *     (Sec. 4.2, the candidate search with its estimate k*m - m - k of the
+ *     Add/Sub saved by a common term of m members reused k times): the most
+ *     reused common pair (two inputs, or inputs and earlier common terms,
+ *     with fixed relative sign) is taken while the estimate is positive,
+ *     the reuse pays for forming it once per tile and LDS rows are left.
+ *     Each common term is formed once per position tile and then enters
+ *     every sum that contains it as a single member;
  *   - uploads the compiled metadata to the current HIP device (synchronous)
  *     unless FIONA_PLAN_HOST_ONLY.
  * The plan keeps a reference to ctx (which must outlive it).  Errors:
@@ -152,12 +162,16 @@ typedef struct fiona_plan_stats_t {
   uint64_t pmult_grouped;          /* PMults after grouping: raw terms + uses */
   uint64_t addsub_unshared;        /* Add/Sub to form every use's signed sum on its own */
   uint64_t addsub_shared;          /* Add/Sub with each distinct sum formed once */
+  uint64_t addsub_partial;         /* Add/Sub after also sharing common partial sums:
+                                      distinct sums plus the common terms themselves */
   uint32_t tile;                   /* coefficients per workgroup */
   uint32_t waves;                  /* wavefronts per workgroup */
   uint32_t lds_bytes;              /* LDS per workgroup */
   uint32_t grid;                   /* workgroups per launch */
   uint32_t split_outputs;          /* outputs split into segments over several wavefronts */
   uint32_t segment_slots;          /* LDS rows holding the segments' partial residues */
+  uint32_t n_partial;              /* common partial sums, each formed once per tile in LDS */
+  uint32_t partial_levels;         /* longest chain of common terms built from common terms */
 } fiona_plan_stats_t;
 
 int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);

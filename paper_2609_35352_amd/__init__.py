@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(_HERE, "libfiona.so")
 FIONA_PLAN_NO_SHARING = 1
 FIONA_PLAN_HOST_ONLY = 2
 FIONA_PLAN_NO_LDS_SUMS = 4
+FIONA_PLAN_NO_PARTIAL_SHARING = 8
 
 STATUS = {0: "FIONA_OK", -1: "FIONA_ERR_ARG", -2: "FIONA_ERR_PLAN", -3: "FIONA_ERR_UNSUPPORTED",
           -4: "FIONA_ERR_ALIGN", -5: "FIONA_ERR_ALIAS", -6: "FIONA_ERR_HIP", -7: "FIONA_ERR_NOMEM",
@@ -49,8 +50,9 @@ class _LayerDesc(ctypes.Structure):
 class _Stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "ct_terms", "n_pmult", "n_member", "n_member_nonzero", "n_use", "n_sum_distinct", "n_sum_resident",
-        "pmult_per_contribution", "pmult_grouped", "addsub_unshared", "addsub_shared")] + \
-        [(n, ctypes.c_uint32) for n in ("tile", "waves", "lds_bytes", "grid", "split_outputs", "segment_slots")]
+        "pmult_per_contribution", "pmult_grouped", "addsub_unshared", "addsub_shared", "addsub_partial")] + \
+        [(n, ctypes.c_uint32) for n in ("tile", "waves", "lds_bytes", "grid", "split_outputs", "segment_slots",
+                                        "n_partial", "partial_levels")]
 
 
 _lib = None

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <map>
 #include <new>
+#include <unordered_map>
 #include <vector>
 
 #include "fiona.h"
@@ -62,6 +63,8 @@ struct fiona_plan {
   const fiona_ctx *ctx = nullptr;
   uint32_t n_in = 0, n_out = 0, n_pt = 0, n_scale = 0, n_member_desc = 0;
   uint32_t n_mat = 0;
+  uint32_t n_part = 0, n_levels = 0;   // common partial sums and their levels
+  std::vector<uint32_t> part_levels;
   uint32_t flags = 0;
   fiona_plan_stats_t st{};
   std::vector<uint4> items;
@@ -165,17 +168,98 @@ int validate_desc(const fiona_layer_desc *d) {
   return FIONA_OK;
 }
 
+// A member of a signed sum or of a common partial sum: an LDS row (an input,
+// or a common partial sum at row n_in + p), the index of the sign that this
+// member's run-time sign is read from, and its sign when the plan was made.
+struct MemberRef {
+  uint32_t row, slot;
+  int32_t sign;
+};
+
 struct SumBuild {
-  std::vector<uint2> members;  // (input, index into the sign array) of the representative
-  bool flip = false;           // representative's canonicalisation flipped its signs
+  std::vector<MemberRef> members;   // of the representative group, sorted by row
+  bool flip = false;                // representative's canonicalisation flipped its signs
   uint32_t n_use = 0;
   uint32_t slot = fiona::kInlineSum;
-  uint32_t mem_begin = 0;
-  uint32_t word_begin = 0;   // header word, then the member words
+  uint32_t word_begin = 0;          // header word, then the member words
 };
+
+// A common partial sum: first + rel * second (rows as in MemberRef).  Its two
+// members' slots are those of the first sum it was found in; at run time its
+// value is normalised by the first member's sign.
+struct PartialBuild {
+  MemberRef first, second;
+  uint32_t level = 1;
+};
+
+constexpr uint32_t kMaxPartialLevels = fiona::kMaxLevels;   // barriers between levels of common terms per tile
+// A common term costs its reduction to a residue and an LDS row once per tile
+// (about as much work as a dozen member additions) before it saves anything.
+constexpr uint64_t kMinPartialReuse = 16;
+
+// Sec. 4.2 candidate search, greedy: repeatedly take the signed pair that
+// the most sum evaluations contain, if the paper's estimate k*m - m - k of the
+// Add/Sub it saves (m = 2 members, k = evaluations containing it) is positive,
+// k reaches kMinPartialReuse and an LDS row is left.  A pair may combine
+// earlier common terms (the level counts how deep); each sum then holds the
+// common term once in place of the two members (so overlapping candidates
+// never both apply to one sum).
+void find_partial_sums(std::vector<SumBuild> &sums, const std::vector<uint64_t> &weight, uint32_t n_in,
+                       uint32_t max_rows, std::vector<PartialBuild> &parts) {
+  std::vector<uint32_t> level_of;   // per partial
+  auto level = [&](uint32_t row) { return row < n_in ? 0u : level_of[row - n_in]; };
+  std::unordered_map<uint64_t, uint64_t> count;
+  while (parts.size() < max_rows) {
+    count.clear();
+    for (size_t s = 0; s < sums.size(); ++s) {
+      const auto &m = sums[s].members;
+      for (size_t i = 0; i < m.size(); ++i)
+        for (size_t j = i + 1; j < m.size(); ++j) {
+          if (std::max(level(m[i].row), level(m[j].row)) + 1 > kMaxPartialLevels) continue;
+          const uint64_t key = ((uint64_t)m[i].row << 33) | ((uint64_t)m[j].row << 1) | (m[i].sign != m[j].sign);
+          count[key] += weight[s];
+        }
+    }
+    uint64_t best = 0, best_k = 0;
+    for (const auto &kv : count)
+      if (kv.second > best_k || (kv.second == best_k && kv.first < best)) {
+        best = kv.first;
+        best_k = kv.second;
+      }
+    const uint64_t m = 2, k = best_k;
+    if (k * m <= m + k || k < kMinPartialReuse) break;
+    const uint32_t ra = (uint32_t)(best >> 33), rb = (uint32_t)((best >> 1) & 0xFFFFFFFFu);
+    const int32_t rel = (best & 1) ? -1 : 1;
+    const uint32_t row = n_in + (uint32_t)parts.size();
+    bool first_use = true;
+    PartialBuild pb;
+    for (auto &sb : sums) {
+      auto &mm = sb.members;
+      size_t ia = mm.size(), ib = mm.size();
+      for (size_t t = 0; t < mm.size(); ++t) {
+        if (mm[t].row == ra) ia = t;
+        if (mm[t].row == rb) ib = t;
+      }
+      if (ia == mm.size() || ib == mm.size() || mm[ia].sign * mm[ib].sign != rel) continue;
+      if (first_use) {
+        pb.first = MemberRef{ra, mm[ia].slot, 1};
+        pb.second = MemberRef{rb, mm[ib].slot, rel};
+        first_use = false;
+      }
+      const MemberRef joined{row, mm[ia].slot, mm[ia].sign};
+      mm.erase(mm.begin() + std::max(ia, ib));
+      mm.erase(mm.begin() + std::min(ia, ib));
+      mm.push_back(joined);   // rows of common terms are above every input row
+    }
+    pb.level = std::max(level(ra), level(rb)) + 1;
+    level_of.push_back(pb.level);
+    parts.push_back(pb);
+  }
+}
 
 int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   const bool share = !(d->flags & FIONA_PLAN_NO_SHARING);
+  const bool partial = share && !(d->flags & FIONA_PLAN_NO_PARTIAL_SHARING);
   const uint32_t n_pm = d->pm_off[d->n_out];
   const uint32_t n_group = d->grp_off[d->n_out];
   P->n_member_desc = n_group ? d->grp_mem_off[n_group] : 0;
@@ -209,7 +293,8 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
           sid = (uint32_t)sums.size();
           SumBuild sb;
           sb.flip = flip;
-          for (auto &pr : part) sb.members.push_back(make_uint2((uint32_t)(pr.first >> 1), pr.second));
+          for (auto &pr : part)
+            sb.members.push_back(MemberRef{(uint32_t)(pr.first >> 1), pr.second, (pr.first & 1) ? -1 : 1});
           sums.push_back(std::move(sb));
           if (share) index.emplace(std::move(key), sid);
         } else {
@@ -220,6 +305,8 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
       }
     }
   }
+  uint64_t addsub_shared = 0;
+  for (const auto &sb : sums) addsub_shared += sb.members.size() - 1;
 
   // Candidates for LDS residency: sums used more than once, most used first.
   const bool lds_sums = !(d->flags & FIONA_PLAN_NO_LDS_SUMS);
@@ -229,11 +316,30 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   std::stable_sort(cand.begin(), cand.end(),
                    [&](uint32_t a, uint32_t b) { return sums[a].n_use > sums[b].n_use; });
   const uint32_t lds_free = kMaxInputs - d->n_in - 1;   // slots left after the inputs and the zero row
-  // One workgroup per CU when the LDS image exceeds half the CU: then 16 wavefronts.
-  const uint32_t est_slots = d->n_in + std::min<uint32_t>((uint32_t)cand.size(), lds_free);
-  P->nw = est_slots * 2 > kMaxInputs ? 16 : 8;
+  if (cand.size() > lds_free) cand.resize(lds_free);
   std::vector<char> resident(sums.size(), 0);
-  for (size_t c = 0; c < cand.size() && c < lds_free; ++c) resident[cand[c]] = 1;
+  for (uint32_t s : cand) resident[s] = 1;
+
+  // Common partial sums in the LDS rows that residency leaves free.  A sum is
+  // evaluated once per tile if resident, else once per use.
+  // An image of at most half the LDS lets two workgroups share a CU; common
+  // terms do not push an image that fits past that line.
+  std::vector<PartialBuild> parts;
+  if (partial && lds_free > cand.size()) {
+    std::vector<uint64_t> weight(sums.size());
+    for (uint32_t s = 0; s < sums.size(); ++s) weight[s] = resident[s] ? 1 : sums[s].n_use;
+    const uint32_t base_rows = d->n_in + 1 + (uint32_t)cand.size();
+    const uint32_t cap = base_rows * 2 <= kMaxInputs ? kMaxInputs / 2 : kMaxInputs;
+    if (cap > base_rows) find_partial_sums(sums, weight, d->n_in, cap - base_rows, parts);
+  }
+  const uint32_t n_part = (uint32_t)parts.size();
+  uint64_t addsub_partial = n_part;   // one Add/Sub forms each common pair
+  for (const auto &sb : sums) addsub_partial += sb.members.size() - 1;
+  const uint32_t rows_free = lds_free - n_part;   // for resident sums and segments
+
+  // One workgroup per CU when the LDS image exceeds half the CU: then 16 wavefronts.
+  const uint32_t est_slots = d->n_in + n_part + std::min<uint32_t>((uint32_t)cand.size(), rows_free);
+  P->nw = est_slots * 2 > kMaxInputs ? 16 : 8;
 
   // Work items: whole outputs, or segments of outputs that are long compared
   // with the share of one wavefront.
@@ -257,23 +363,55 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
     uint32_t S = (uint32_t)(out_cost[j] / target + 0.5);
     S = std::min<uint32_t>(S, (uint32_t)(out_cost[j] / kMinSegmentCost));
     S = std::min<uint32_t>(S, kMaxSegments);
-    if (S >= 2 && seg_slots + S <= lds_free) {
+    if (S >= 2 && seg_slots + S <= rows_free) {
       nseg[j] = S;
       seg_slots += S;
     }
   }
   P->n_seg_slots = seg_slots;
-  if (cand.size() > lds_free - seg_slots) cand.resize(lds_free - seg_slots);
-
-  // device records: members of every distinct sum, resident sums, uses per output
-  uint64_t addsub_shared = 0;
-  for (auto &sb : sums) {
-    sb.mem_begin = (uint32_t)P->members.size();
-    sb.word_begin = (uint32_t)P->sums_dev.size() * fiona::kSumWords;
-    for (auto &m : sb.members) P->members.push_back(m);
-    P->sums_dev.push_back(make_uint2(sb.mem_begin, (uint32_t)sb.members.size()));
-    addsub_shared += sb.members.size() - 1;
+  if (cand.size() > rows_free - seg_slots) {   // segments take precedence over the least used residents
+    for (size_t c = rows_free - seg_slots; c < cand.size(); ++c) resident[cand[c]] = 0;
+    cand.resize(rows_free - seg_slots);
   }
+
+  // Device records.  Words: one block per common partial sum, then one per
+  // distinct signed sum; the sign-packing kernel fills them on every call.
+  for (uint32_t p = 0; p < n_part; ++p) {
+    const uint32_t mb = (uint32_t)P->members.size();
+    P->members.push_back(make_uint2(parts[p].first.row, parts[p].first.slot));
+    P->members.push_back(make_uint2(parts[p].second.row, parts[p].second.slot));
+    P->sums_dev.push_back(make_uint2(mb, 2u | fiona::kNormaliseSigns));
+  }
+  for (auto &sb : sums) {
+    const uint32_t mb = (uint32_t)P->members.size();
+    sb.word_begin = (uint32_t)P->sums_dev.size() * fiona::kSumWords;
+    for (auto &m : sb.members) P->members.push_back(make_uint2(m.row, m.slot));
+    P->sums_dev.push_back(make_uint2(mb, (uint32_t)sb.members.size()));
+  }
+  // Rows of common terms are numbered level by level (a term only reads rows
+  // of lower levels), so each level is formed after a barrier; part_levels[l]
+  // is the end of the rows of level l+1.
+  P->n_part = n_part;
+  uint32_t n_levels = 0;
+  {
+    std::vector<uint32_t> order(n_part);
+    for (uint32_t p = 0; p < n_part; ++p) order[p] = p;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](uint32_t a, uint32_t b) { return parts[a].level < parts[b].level; });
+    std::vector<uint32_t> new_row(n_part);
+    for (uint32_t t = 0; t < n_part; ++t) new_row[order[t]] = t;
+    for (auto &m : P->members)
+      if (m.x >= d->n_in) m.x = d->n_in + new_row[m.x - d->n_in];
+    const std::vector<uint2> blocks(P->sums_dev.begin(), P->sums_dev.begin() + n_part);
+    for (uint32_t p = 0; p < n_part; ++p) P->sums_dev[new_row[p]] = blocks[p];
+    P->part_levels.assign(kMaxPartialLevels, 0);
+    for (uint32_t t = 0; t < n_part; ++t) {
+      const uint32_t lv = parts[order[t]].level;
+      n_levels = std::max(n_levels, lv);
+      for (uint32_t l = lv - 1; l < kMaxPartialLevels; ++l) P->part_levels[l] = t + 1;
+    }
+  }
+  P->n_levels = n_levels;
   for (uint32_t s : cand) {
     sums[s].slot = (uint32_t)P->mats.size();
     P->mats.push_back(sums[s].word_begin);
@@ -287,12 +425,16 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
       P->uses.push_back(make_uint4(sb.word_begin, sb.slot, u.scale | (u.neg ? 0x80000000u : 0u), 0));
     }
   }
+  P->st.addsub_partial = addsub_partial;
+  P->st.n_partial = n_part;
+  P->st.partial_levels = n_levels;
+
   // Raw-term records, per work item, in chunks of at most kChunkTerms terms
   // (one block of kChunkSlots records each, see hybrid_kernel.hpp).  The
   // terms of an output may be taken in any order (the sum is exact), so they
   // are sorted by plaintext offset: a chunk then covers a short stretch of the
   // plaintext table, and its terms' offsets from the chunk base fit 31 bits.
-  const uint32_t zero_row = d->n_in + (uint32_t)P->mats.size() + seg_slots;
+  const uint32_t zero_row = d->n_in + n_part + (uint32_t)P->mats.size() + seg_slots;
   const uint64_t ln8 = (uint64_t)P->ctx->L * P->ctx->N * 8;
   auto emit_chunks = [&](const std::vector<std::pair<uint64_t, uint32_t>> &terms, size_t t0, size_t t1) {
     const uint32_t first = (uint32_t)(P->pm.size() / fiona::kChunkSlots);
@@ -466,7 +608,7 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   }
   P->tiles = (ctx->N + fiona::kTile - 1) / fiona::kTile;
   P->grid = P->tiles * ctx->L;
-  P->lds_bytes = (P->n_in + P->n_mat + P->n_seg_slots + 1) * kSlotBytes;
+  P->lds_bytes = (P->n_in + P->n_part + P->n_mat + P->n_seg_slots + 1) * kSlotBytes;
   P->st.tile = fiona::kTile;
   P->st.waves = P->nw;
   P->st.split_outputs = (uint32_t)P->splits.size();
@@ -479,7 +621,10 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   k.n_in = P->n_in;
   k.n_mat = P->n_mat;
   k.n_split = (uint32_t)P->splits.size();
-  k.zero_row = P->n_in + P->n_mat + P->n_seg_slots;
+  k.zero_row = P->n_in + P->n_part + P->n_mat + P->n_seg_slots;
+  k.n_part = P->n_part;
+  k.n_levels = P->n_levels;
+  for (uint32_t l = 0; l < fiona::kMaxLevels; ++l) k.level_end[l] = P->part_levels[l];
   k.tiles = P->tiles;
   if (!(desc->flags & FIONA_PLAN_HOST_ONLY)) {
     rc = upload_plan(P);

@@ -5,8 +5,11 @@
 // NTT domain, so a tile needs no data from any other tile.  Per tile:
 //   1. each input ciphertext's two polynomials are read once from HBM and kept
 //      in LDS as radix-2^25 digits (16 B per input and lane);
-//   2. the signed sums that several outputs share are formed once, by Add/Sub
-//      of LDS-resident inputs, and kept in LDS (Sec. 4.2 "Sharing Signed Sums");
+//   2. signed terms common to several sums (partial overlaps) are formed once,
+//      reduced to residues and kept in LDS as extra rows (Sec. 4.2, the
+//      sharing candidates); the signed sums that several outputs share are
+//      formed once, by Add/Sub of LDS rows, and kept in LDS (Sec. 4.2
+//      "Sharing Signed Sums");
 //   3. each wavefront works through its list of work items.  An item is one
 //      output, or one segment of a long output: its raw terms stream their
 //      plaintext slices from HBM (each plaintext word feeds the products with
@@ -35,10 +38,12 @@ constexpr uint32_t kInlineSum = 0xFFFFFFFFu;
 constexpr uint32_t kRawBatch = 8;         // plaintext loads per batch; two batches in flight
 constexpr uint32_t kRawBatches = kChunkTerms / kRawBatch;   // batches per chunk of raw records
 constexpr uint32_t kChunkSlots = 64;      // records per chunk block; the last one is the header
-constexpr uint32_t kSumBatch = 8;         // member reads issued before their additions
+constexpr uint32_t kSumBatch = 4;         // member reads issued before their additions
 constexpr uint32_t kSumBatches = kMaxMembers / kSumBatch;
 constexpr uint32_t kSumWords = 64;        // words per distinct sum: header + padded member rows
 constexpr uint32_t kSegmentFlag = 0x80000000u;
+constexpr uint32_t kNormaliseSigns = 0x80000000u;   // block flag: signs relative to the first member's
+constexpr uint32_t kMaxLevels = 4;        // levels of common partial sums
 constexpr int kLoadNT = 2;                // cache policy of the plaintext stream: nontemporal
 static_assert(kChunkTerms % kRawBatch == 0 && kChunkTerms < kChunkSlots, "chunk layout");
 // header, rows to add from word 1 up, rows to subtract from word 62 down, each list padded to a batch
@@ -49,42 +54,49 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // Per-call description for the sign-packing kernel.
 struct PackParams {
   const int8_t *signs;      // [n_member of the layer description]
-  const uint2 *members;     // per member: input index, index into signs
-  const uint2 *sums;        // per distinct sum: member begin, member count (<= kMaxMembers)
-  uint32_t *words;          // per sum: kSumWords words
+  const uint2 *members;     // per member: LDS row, index into signs
+  const uint2 *sums;        // per block: member begin, member count (<= kMaxMembers) | kNormaliseSigns
+  uint32_t *words;          // per block: kSumWords words
   uint32_t n_sums, zero_row;
 };
 
-// Scalars of the main kernel.
+// Scalars of the main kernel.  LDS rows: inputs, common partial sums (level by
+// level; level l ends at level_end[l]), resident signed sums, segment slots,
+// the zero row.
 struct KShape {
-  uint32_t N, L, n_in, n_mat, n_split, zero_row, tiles;
+  uint32_t N, L, n_in, n_part, n_levels, n_mat, n_split, zero_row, tiles;
+  uint32_t level_end[kMaxLevels];
 };
 
 __device__ __forceinline__ uint64_t pair64(uint32_t lo, uint32_t hi) { return ((uint64_t)hi << 32) | lo; }
-__device__ __forceinline__ uint32_t pad8(uint32_t n) { return (n + 7u) & ~7u; }
+__device__ __forceinline__ uint32_t pad_batch(uint32_t n) { return (n + kSumBatch - 1) & ~(kSumBatch - 1); }
 __device__ __forceinline__ uint32_t bcast(uint32_t v, uint32_t l) { return __builtin_amdgcn_readlane(v, l); }
 
-// The words of every distinct signed sum for this call.  Word 0 holds the
-// numbers of rows to add and to subtract, each rounded up to a batch of 8;
-// the rows to add follow from word 1 upwards and the rows to subtract from
-// word 62 downwards, each list padded with the all-zero row.  A row is given
-// as its LDS byte offset.  Members whose run-time sign is 0 are left out
-// (Sec. 3 Obs. 2, the skip).  One wavefront per sum.
+// The words of every common partial sum and distinct signed sum for this
+// call.  Word 0 holds the numbers of rows to add and to subtract, each
+// rounded up to a batch of kSumBatch; the rows to add follow from word 1 upwards and
+// the rows to subtract from word 62 downwards, each list padded with the
+// all-zero row.  A row is given as its LDS byte offset.  Members whose
+// run-time sign is 0 are left out (Sec. 3 Obs. 2, the skip).  A common
+// partial sum takes its signs relative to its first member's, so it is the
+// same term in every sum that contains it.  One wavefront per block.
 __global__ void __launch_bounds__(256) pack_members_kernel(const PackParams P) {
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t s = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (s >= P.n_sums) return;
   const uint2 sm = P.sums[s];
+  const uint32_t cnt = sm.y & ~kNormaliseSigns;
+  const int32_t h0 = (sm.y & kNormaliseSigns) ? (int32_t)P.signs[P.members[sm.x].y] : 1;
   uint32_t cls = 3, row = 0;
-  if (lane < sm.y) {
+  if (lane < cnt) {
     const uint2 m = P.members[sm.x + lane];
-    const int32_t h = P.signs[m.y];
+    const int32_t h = P.signs[m.y] * h0;
     cls = h > 0 ? 0u : (h < 0 ? 1u : 2u);
     row = m.x;
   }
   const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
   const uint64_t b0 = __ballot(cls == 0), b1 = __ballot(cls == 1);
-  const uint32_t n0 = __popcll(b0), n1 = __popcll(b1), p0 = pad8(n0), p1 = pad8(n1);
+  const uint32_t n0 = __popcll(b0), n1 = __popcll(b1), p0 = pad_batch(n0), p1 = pad_batch(n1);
   uint32_t *w = P.words + (size_t)s * kSumWords;
   if (cls == 0) w[1 + __popcll(b0 & below)] = row * kRowBytes;
   if (cls == 1) w[62 - __popcll(b1 & below)] = row * kRowBytes;
@@ -98,7 +110,7 @@ __device__ __forceinline__ const uint4 &lds_row(const uint4 *lds, uint32_t row_b
   return *(const uint4 *)((const char *)lds + row_bytes + lane_bytes);
 }
 
-// Adds the rows at word lanes first + step * u (u = 0..7) into the packed digit sums.
+// Adds the rows at word lanes first + step * u (u < kSumBatch) into the packed digit sums.
 template <int First, int Step>
 __device__ __forceinline__ void sum_batch(uint64_t &a, uint64_t &b, uint32_t wv, const uint4 *lds, uint32_t lane16) {
   uint4 x[kSumBatch];
@@ -124,7 +136,7 @@ __device__ __forceinline__ void sum_rows(uint32_t np, uint32_t nn, uint64_t &pa,
 // Signed sum U = sum h x of one distinct sum whose words are in wv (one per
 // lane), digit-wise: (U0, U1) for each polynomial.  The two 25-bit digits of
 // an input are added as one 64-bit word (the halves never carry into each
-// other for at most 48 members), in batches of 8 LDS reads.
+// other for at most 48 members), in batches of kSumBatch LDS reads.
 __device__ __forceinline__ uint4 signed_sum(uint32_t wv, const uint4 *lds, uint32_t lane16) {
   const uint32_t hdr = bcast(wv, 0);
   uint64_t pa = 0, pb = 0, na = 0, nb = 0;
@@ -213,7 +225,7 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
     const uint32_t *__restrict__ dest, const uint2 *__restrict__ waves, const uint4 *__restrict__ splits,
     const uint2 *__restrict__ pm, const uint4 *__restrict__ uses, const uint32_t *__restrict__ mats,
     const uint32_t *__restrict__ words, const KShape S) {
-  extern __shared__ uint4 lds[];   // [n_in + n_mat + segment slots + zero row][kTile]
+  extern __shared__ uint4 lds[];   // [n_in + n_part + n_mat + segment slots + zero row][kTile]
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t lane16 = lane * 16u;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -236,13 +248,28 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
   if (wave == NW - 1) lds[S.zero_row * kTile + lane] = make_uint4(0, 0, 0, 0);   // padding row
   __syncthreads();
 
-  // 2. shared signed sums, formed once per tile
-  uint4 *sums = lds + (size_t)S.n_in * kTile;
+  // 2. common partial sums, level by level, each kept as a canonical residue
+  // in the inputs' digit form so that it enters other sums as one member
+  uint4 *parts = lds + (size_t)S.n_in * kTile;
+  for (uint32_t lv = 0, p0 = 0; lv < S.n_levels; ++lv) {
+    const uint32_t p1 = S.level_end[lv];
+    for (uint32_t p = p0 + wave; p < p1; p += NW) {
+      const uint4 U = signed_sum(words[(size_t)p * kSumWords + lane], lds, lane16);
+      const uint64_t v0 = reduce_i64((int64_t)(int32_t)U.x + ((int64_t)(int32_t)U.y << 25), lc.q, lc.qinv);
+      const uint64_t v1 = reduce_i64((int64_t)(int32_t)U.z + ((int64_t)(int32_t)U.w << 25), lc.q, lc.qinv);
+      parts[p * kTile + lane] = make_uint4(lo_digit(v0), hi_digit(v0), lo_digit(v1), hi_digit(v1));
+    }
+    p0 = p1;
+    __syncthreads();
+  }
+
+  // 3. shared signed sums, formed once per tile
+  uint4 *sums = parts + (size_t)S.n_part * kTile;
   for (uint32_t s = wave; s < S.n_mat; s += NW)
     sums[s * kTile + lane] = signed_sum(words[(size_t)mats[s] + lane], lds, lane16);
   __syncthreads();
 
-  // 3. this wavefront's work items; the first records of each item are loaded
+  // 4. this wavefront's work items; the first records of each item are loaded
   // while the previous item runs
   uint4 *segs = sums + (size_t)S.n_mat * kTile;
   const char *pt_tile = (const char *)(pt + (size_t)limb * S.N + k0);
@@ -320,7 +347,7 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
     }
   }
 
-  // 4. outputs that were split across wavefronts: add their segments' residues
+  // 5. outputs that were split across wavefronts: add their segments' residues
   if (S.n_split) {
     __syncthreads();
     for (uint32_t s = wave; s < S.n_split; s += NW) {

@@ -174,5 +174,43 @@ def test_config_plans(name):
     if name == "vit768":
         assert st["n_sum_distinct"] <= 48 and st["n_sum_resident"] == st["n_sum_distinct"]
     assert st["grid"] == lay.L * lay.N // 64
-    assert st["lds_bytes"] == (lay.n_in + st["n_sum_resident"] + st["segment_slots"] + 1) * 1024 <= 160 * 1024
+    assert st["lds_bytes"] == (lay.n_in + st["n_partial"] + st["n_sum_resident"] + st["segment_slots"] + 1) * 1024 <= 160 * 1024
     assert st["waves"] in (8, 16)
+
+
+def test_partial_sharing_finds_common_terms():
+    """Sec. 4.2 candidate search: groups of one layer that only partly overlap
+    share common signed pairs; the estimate k*m - m - k decides."""
+    cfg = synth.LayerConfig("partial_share", N=256, L=2, n_in=16, n_out=48, T=96, g=12, ternary=0.95)
+    lay = synth.make_layer(cfg, 5, moduli=synth.ntt_primes(256, 2))
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    st = fiona.Plan.from_layer(ctx, lay, flags=HOST).stats()
+    assert st["n_partial"] > 0 and st["partial_levels"] >= 2
+    # one Add/Sub forms each common pair; every sum that holds it saves one
+    assert st["addsub_partial"] < st["addsub_shared"] <= st["addsub_unshared"]
+    assert st["lds_bytes"] == (lay.n_in + st["n_partial"] + st["n_sum_resident"] + st["segment_slots"] + 1) * 1024
+    off = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_NO_PARTIAL_SHARING).stats()
+    assert off["n_partial"] == 0 and off["addsub_partial"] == off["addsub_shared"] == st["addsub_shared"]
+    none = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_NO_SHARING).stats()
+    assert none["n_partial"] == 0 and none["n_sum_distinct"] == none["n_use"]
+
+
+def test_partial_sharing_worked_pair():
+    """Three sums over inputs 0..3 that all contain A0 - A1 (20 uses each, so
+    k = 60): the pair is formed once, and each sum holds it as one member."""
+    q = synth.ntt_primes(16, 1)
+    ctx = fiona.Ctx(16, 1, q)
+    groups = [([0, 1, 2], [1, -1, 1]), ([0, 1, 3], [-1, 1, 1]), ([0, 1, 2, 3], [1, -1, -1, 1])] * 20
+    mem_in, mem_sg, gm = [], [], [0]
+    for ins, sg in groups:
+        mem_in += ins
+        mem_sg += sg
+        gm.append(len(mem_in))
+    n_out = len(groups)
+    args = dict(n_in=4, n_out=n_out, n_pt=0, n_scale=n_out, pm_off=[0] * (n_out + 1), pm_input=[], pm_pt=[],
+                grp_off=list(range(n_out + 1)), grp_mem_off=gm, mem_input=mem_in, mem_sign=mem_sg,
+                grp_scale=list(range(n_out)))
+    st = fiona.Plan(ctx, flags=HOST | fiona.FIONA_PLAN_NO_LDS_SUMS, **args).stats()
+    assert st["n_sum_distinct"] == 3 and st["n_partial"] >= 1
+    # the three distinct sums need 2 + 2 + 3 Add/Sub; with A0 - A1 shared: 1 + 1 + 1 + 2 (+ 1 to form it)
+    assert st["addsub_shared"] == 7 and st["addsub_partial"] <= 5

@@ -91,6 +91,7 @@ SMALL = {
     "lds_full": synth.LayerConfig("lds_full", N=128, L=1, n_in=159, n_out=4, T=318, g=53, ternary=0.5, pool=2),
     "all_ternary": synth.LayerConfig("all_ternary", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=1.0, pool=3),
     "all_raw": synth.LayerConfig("all_raw", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=0.0),
+    "partial_share": synth.LayerConfig("partial_share", N=256, L=2, n_in=16, n_out=48, T=96, g=12, ternary=0.95),
 }
 
 
@@ -113,10 +114,13 @@ def test_small_layer_elementwise(dev, name):
     _assert_equal(_host(out_t, layer), expect, name)
 
 
-@pytest.mark.parametrize("flags", [fiona.FIONA_PLAN_NO_SHARING, fiona.FIONA_PLAN_NO_LDS_SUMS,
-                                   fiona.FIONA_PLAN_NO_SHARING | fiona.FIONA_PLAN_NO_LDS_SUMS])
-def test_plan_variants_agree(dev, flags):
-    layer = _small_layer("ragged_pool")
+@pytest.mark.parametrize("name,flags", [("ragged_pool", fiona.FIONA_PLAN_NO_SHARING),
+                                        ("ragged_pool", fiona.FIONA_PLAN_NO_LDS_SUMS),
+                                        ("ragged_pool", fiona.FIONA_PLAN_NO_SHARING | fiona.FIONA_PLAN_NO_LDS_SUMS),
+                                        ("partial_share", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
+                                        ("partial_share", fiona.FIONA_PLAN_NO_LDS_SUMS)])
+def test_plan_variants_agree(dev, name, flags):
+    layer = _small_layer(name)
     x, pt = synth.input_values(layer), synth.pt_values(layer)
     expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
     out_t, *_ = _run(layer, dev, x, pt, flags=flags)
