@@ -78,6 +78,7 @@ def time_layer(layer, dev, steps, warmup, stream, label):
     total_ms = 0.0
     total_bytes = 0
     per_chunk = []
+    waves = set()
     for ci, sub in enumerate(subs):
         synth.gpu.fill_pts(sub, pt_t)
         plan = fiona.Plan.from_layer(ctx, sub)
@@ -101,12 +102,14 @@ def time_layer(layer, dev, steps, warmup, stream, label):
         total_ms += ms
         total_bytes += nbytes
         per_chunk.append({"outputs": sub.n_out, "ms": round(ms, 4), "alg_GBps": round(nbytes / ms / 1e6, 1)})
+        waves.add(plan.stats()["waves"])
         if ci == 0 or ci == len(subs) - 1 or ci % 8 == 0:
             log("[bench] %s chunk %d/%d: %.3f ms/launch, %.1f GB/s algorithmic, plan %s"
                 % (label, ci + 1, len(subs), ms, nbytes / ms / 1e6, plan.stats()))
         del plan
     del pt_t, out_t, in_t
     torch.cuda.empty_cache()
+    time_layer.kernels = ["hybrid_linear_kernel<%d>" % w for w in sorted(waves)]
     return total_ms, total_bytes, per_chunk
 
 
@@ -187,6 +190,7 @@ def main():
                           "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "chunks": ap_chunks}), flush=True)
         return
     hy_ms, hy_bytes, hy_chunks = time_layer(layer, dev, args.steps, args.warmup, stream, "hybrid")
+    hy_kernels = time_layer.kernels
     torch.cuda.synchronize()
     hy_value = layer.ct_terms / (hy_ms * 1e-3)
     hy_gbs = hy_bytes / hy_ms / 1e6
@@ -225,7 +229,7 @@ def main():
                      "frac": round(hy_gbs / HBM_PEAK_GBS, 4),
                      "traffic": None if traffic is None else round(traffic),
                      "alg_bytes_per_launch": hy_bytes // n_launch,
-                     "kernel": "hybrid_linear_kernel<8>"},
+                     "kernel": " + ".join(hy_kernels)},
         "all_pmult": allpm,
         "hybrid_chunks": hy_chunks if n_launch > 1 else None,
         "gpu_wall_s": round(wall, 2),
