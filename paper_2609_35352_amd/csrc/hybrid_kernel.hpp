@@ -152,7 +152,8 @@ __device__ __forceinline__ uint4 signed_sum(uint32_t wv, const uint4 *lds, uint3
 // last lane) is {chunk base bits 0..31, bits 32..47 | nb << 16}; the chunk
 // base is a byte offset into the plaintext table.  The plaintext of record r
 // is read with a buffer load: descriptor base = this tile's plaintext column
-// at the chunk base, lane offset in a VGPR, record offset in an SGPR.
+// at the chunk base, and lane offset plus record offset in one VGPR (an
+// SGPR offset that changes from load to load streams measurably slower).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const char *pt_tile, uint2 rec, uint32_t &nb) {
   const uint32_t lo = bcast(rec.x, kChunkSlots - 1), hi = bcast(rec.y, kChunkSlots - 1);
   nb = hi >> 16;
@@ -165,19 +166,22 @@ __device__ __forceinline__ void raw_issue(u32x2 (&w)[kRawBatch], __amdgpu_buffer
                                           uint32_t voff) {
 #pragma unroll
   for (uint32_t u = 0; u < kRawBatch; ++u)
-    w[u] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, bcast(rec.x, r0 + u), kLoadNT);
+    w[u] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + bcast(rec.x, r0 + u), 0, kLoadNT);
 }
 
 // Multiply-accumulate the batch of records r0 .. r0+7, whose plaintext words are in w.
 __device__ __forceinline__ void raw_consume(Acc &a0, Acc &a1, const u32x2 (&w)[kRawBatch], uint2 rec, uint32_t r0,
                                             const uint4 *lds, uint32_t lane16) {
-  uint4 x[kRawBatch];
 #pragma unroll
-  for (uint32_t u = 0; u < kRawBatch; ++u) x[u] = lds_row(lds, bcast(rec.y, r0 + u), lane16);
+  for (uint32_t h = 0; h < kRawBatch; h += 4) {
+    uint4 x[4];
 #pragma unroll
-  for (uint32_t u = 0; u < kRawBatch; ++u) {
-    mac(a0, x[u].x, x[u].y, w[u].x, w[u].y);
-    mac(a1, x[u].z, x[u].w, w[u].x, w[u].y);
+    for (uint32_t u = 0; u < 4; ++u) x[u] = lds_row(lds, bcast(rec.y, r0 + h + u), lane16);
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) {
+      mac(a0, x[u].x, x[u].y, w[h + u].x, w[h + u].y);
+      mac(a1, x[u].z, x[u].w, w[h + u].x, w[h + u].y);
+    }
   }
 }
 
