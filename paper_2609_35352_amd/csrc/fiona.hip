@@ -676,20 +676,26 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return FIONA_ERR_ARG;
   const uint32_t n_sums = (uint32_t)plan->sums_dev.size();
-  if (n_sums) {   // this call's signs: the words of every distinct sum
+  const uint32_t n_uses = (uint32_t)plan->uses.size();
+  if (n_sums) {   // this call's signs and scales: the word blocks and the uses' signed scales
     PackParams pp;
     pp.signs = ternary_groups;
     pp.members = plan->d_members;
     pp.sums = plan->d_sums;
     pp.words = plan->d_words;
+    pp.scales = scales;
+    pp.uses = const_cast<uint4 *>(plan->d_uses);
     pp.n_sums = n_sums;
     pp.zero_row = plan->shape.zero_row;
-    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((n_sums + 3) / 4), dim3(256), 0, stream, pp);
+    pp.n_uses = n_uses;
+    pp.sum_blocks = (n_sums + 3) / 4;
+    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3(pp.sum_blocks + (n_uses + 255) / 256), dim3(256), 0, stream,
+                       pp);
     if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   }
   auto kernel = plan->nw == 16 ? fiona::hybrid_linear_kernel<16> : fiona::hybrid_linear_kernel<8>;
   hipLaunchKernelGGL(kernel, dim3(plan->grid), dim3(plan->nw * 64), plan->lds_bytes, stream, in_cts, pt_diags,
-                     scales, out_cts, plan->d_limbs, plan->d_items, plan->d_dest, plan->d_waves, plan->d_splits,
+                     out_cts, plan->d_limbs, plan->d_items, plan->d_dest, plan->d_waves, plan->d_splits,
                      plan->d_pm, plan->d_uses, plan->d_mats, plan->d_words, plan->shape);
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   return FIONA_OK;

@@ -57,7 +57,9 @@ struct PackParams {
   const uint2 *members;     // per member: LDS row, index into signs
   const uint2 *sums;        // per block: member begin, member count (<= kMaxMembers) | kNormaliseSigns
   uint32_t *words;          // per block: kSumWords words
-  uint32_t n_sums, zero_row;
+  const uint64_t *scales;   // [n_scale of the layer description]
+  uint4 *uses;              // per use: .w receives the signed scale of this call
+  uint32_t n_sums, zero_row, n_uses, sum_blocks;
 };
 
 // Scalars of the main kernel.  LDS rows: inputs, common partial sums (level by
@@ -81,6 +83,15 @@ __device__ __forceinline__ uint32_t bcast(uint32_t v, uint32_t l) { return __bui
 // partial sum takes its signs relative to its first member's, so it is the
 // same term in every sum that contains it.  One wavefront per block.
 __global__ void __launch_bounds__(256) pack_members_kernel(const PackParams P) {
+  if (blockIdx.x >= P.sum_blocks) {   // the signed scale of every use: (-1)^negate * c, c < 2^20
+    const uint32_t u = (blockIdx.x - P.sum_blocks) * 256 + threadIdx.x;
+    if (u < P.n_uses) {
+      const uint32_t z = P.uses[u].z;
+      const int32_t c = (int32_t)P.scales[z & 0x7FFFFFFFu];
+      P.uses[u].w = (uint32_t)((z >> 31) ? -c : c);
+    }
+    return;
+  }
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t s = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (s >= P.n_sums) return;
@@ -224,8 +235,7 @@ __device__ __forceinline__ uint4 load_use_chunk(const uint4 *uses, uint32_t begi
 
 template <int NW>
 __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
-    const uint64_t *__restrict__ in, const uint64_t *__restrict__ pt, const uint64_t *__restrict__ scales,
-    uint64_t *__restrict__ out, const LimbConst *__restrict__ limbs, const uint4 *__restrict__ items,
+    const uint64_t *__restrict__ in, const uint64_t *__restrict__ pt, uint64_t *__restrict__ out, const LimbConst *__restrict__ limbs, const uint4 *__restrict__ items,
     const uint32_t *__restrict__ dest, const uint2 *__restrict__ waves, const uint4 *__restrict__ splits,
     const uint2 *__restrict__ pm, const uint4 *__restrict__ uses, const uint32_t *__restrict__ mats,
     const uint32_t *__restrict__ words, const KShape S) {
@@ -291,9 +301,13 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
       raw_next = item_next.y ? load_chunk(pm, item_next.x, lane) : make_uint2(0, 0);
       use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
     }
-    // member words of this item's first in-place sum
-    uint32_t words_next = 0;
-    if (item.w && bcast(use_rec.y, 0) == kInlineSum) words_next = words[(size_t)bcast(use_rec.x, 0) + lane];
+    // word blocks of this item's first two uses (loaded before the raw route,
+    // so waiting for them never waits for plaintext loads)
+    uint32_t wq0 = 0, wq1 = 0;
+    if (item.w) {
+      wq0 = words[(size_t)bcast(use_rec.x, 0) + lane];
+      wq1 = words[(size_t)(item.w > 1 ? bcast(use_rec.x, 1) : 0u) + lane];
+    }
     Acc a0, a1;
     acc_zero(a0);
     acc_zero(a1);
@@ -313,29 +327,37 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
       raw_chunk(nb, rs, rec, voff, a0, a1, lds, lane16);
     }
 
-    // signed route: each use applies its group's scale once to a signed sum;
-    // the next in-place sum's member words load while this one is added
+    // signed route: each use applies its group's scale once to a signed sum.
+    // Word blocks are loaded two uses ahead, on every path (a resident sum's,
+    // or block 0 past the end, is loaded and not used), so each use waits
+    // only for its own block.
     for (uint32_t base = 0; base < item.w; base += 64) {
       const uint32_t n = min(64u, item.w - base);
-      const uint4 rec = use_rec;   // word begin, LDS slot or kInlineSum, scale | negate << 31, 0
-      if (base + 64 < item.w) use_rec = load_use_chunk(uses, item.z + base + 64, min(64u, item.w - base - 64), lane);
-      const uint32_t scl = lane < n ? (uint32_t)scales[rec.z & 0x7FFFFFFFu] : 0u;   // scales are < 2^20
+      // word begin, LDS slot or kInlineSum, scale index | negate << 31, signed scale
+      const uint4 rec = use_rec;
+      const bool more = base + 64 < item.w;
+      if (more) use_rec = load_use_chunk(uses, item.z + base + 64, min(64u, item.w - base - 64), lane);
       if (base && base % kFoldUses == 0) fold(a0, a1, r0, r1, lc);
-      for (uint32_t r = 0; r < n; ++r) {
+      // word block of use base + j (j < n + 2), or block 0 past the item's end
+      auto block_of = [&](uint32_t j) -> size_t {
+        if (j < n) return bcast(rec.x, j);
+        return more ? bcast(use_rec.x, j - n) : 0u;
+      };
+      auto apply = [&](uint32_t r, uint32_t wq) {
         const uint32_t slot = bcast(rec.y, r);
-        const uint32_t wcur = words_next;
-        if (r + 1 < n) {
-          if (bcast(rec.y, r + 1) == kInlineSum) words_next = words[(size_t)bcast(rec.x, r + 1) + lane];
-        } else if (base + 64 < item.w) {
-          if (bcast(use_rec.y, 0) == kInlineSum) words_next = words[(size_t)bcast(use_rec.x, 0) + lane];
-        }
-        const uint4 U = slot != kInlineSum ? sums[slot * kTile + lane] : signed_sum(wcur, lds, lane16);
-        const uint32_t sc = bcast(rec.z, r);
-        const int32_t cabs = (int32_t)bcast(scl, r);
-        const int32_t c = (sc >> 31) ? -cabs : cabs;
+        const uint4 U = slot != kInlineSum ? sums[slot * kTile + lane] : signed_sum(wq, lds, lane16);
+        const int32_t c = (int32_t)bcast(rec.w, r);
         smac(a0, c, (int32_t)U.x, (int32_t)U.y);
         smac(a1, c, (int32_t)U.z, (int32_t)U.w);
+      };
+      uint32_t r = 0;
+      for (; r + 1 < n; r += 2) {
+        apply(r, wq0);
+        wq0 = words[block_of(r + 2) + lane];
+        apply(r + 1, wq1);
+        wq1 = words[block_of(r + 3) + lane];
       }
+      if (r < n) apply(r, wq0);   // an odd count: only the item's last use chunk
     }
 
     const uint64_t y0 = finish(a0, r0, lc);
