@@ -57,8 +57,11 @@ def measured_traffic(workload: str, variant: str):
     return None if v is None else float(v["bytes_per_launch"])
 
 
-def time_layer(layer, dev, steps, warmup, stream, label):
-    """Run every output chunk of `layer`; return (sum of per-chunk ms per launch, bytes, kernel list)."""
+def time_layer(layer, dev, steps, warmup, stream, label, flags=0):
+    """Run every output chunk of `layer` with plans made under `flags`; return
+    (sum of per-chunk ms per launch, algorithmic bytes, per-chunk records).
+    time_layer.kernels names the kernel instances and time_layer.counts sums
+    the plans' operation counts over the chunks."""
     import torch
     import synth
     import synth.gpu
@@ -79,9 +82,10 @@ def time_layer(layer, dev, steps, warmup, stream, label):
     total_bytes = 0
     per_chunk = []
     waves = set()
+    counts = {}
     for ci, sub in enumerate(subs):
         synth.gpu.fill_pts(sub, pt_t)
-        plan = fiona.Plan.from_layer(ctx, sub)
+        plan = fiona.Plan.from_layer(ctx, sub, flags=flags)
         sign_t = torch.from_numpy(np.ascontiguousarray(sub.mem_sign)).to(dev) if sub.mem_sign.size else \
             torch.zeros(1, dtype=torch.int8, device=dev)
         scale_t = torch.from_numpy(np.ascontiguousarray(sub.scales.view(np.int64))).to(dev) if sub.scales.size \
@@ -102,7 +106,10 @@ def time_layer(layer, dev, steps, warmup, stream, label):
         total_ms += ms
         total_bytes += nbytes
         per_chunk.append({"outputs": sub.n_out, "ms": round(ms, 4), "alg_GBps": round(nbytes / ms / 1e6, 1)})
-        waves.add(plan.stats()["waves"])
+        st = plan.stats()
+        waves.add(st["waves"])
+        for key in ("pmult_grouped", "n_use", "addsub_partial", "n_partial", "n_sum_distinct"):
+            counts[key] = counts.get(key, 0) + st[key]
         if ci == 0 or ci == len(subs) - 1 or ci % 8 == 0:
             log("[bench] %s chunk %d/%d: %.3f ms/launch, %.1f GB/s algorithmic, plan %s"
                 % (label, ci + 1, len(subs), ms, nbytes / ms / 1e6, plan.stats()))
@@ -110,6 +117,7 @@ def time_layer(layer, dev, steps, warmup, stream, label):
     del pt_t, out_t, in_t
     torch.cuda.empty_cache()
     time_layer.kernels = ["hybrid_linear_kernel<%d>" % w for w in sorted(waves)]
+    time_layer.counts = counts
     return total_ms, total_bytes, per_chunk
 
 
@@ -147,6 +155,8 @@ def main():
     ap.add_argument("--no-allpmult", action="store_true", help="time only the hybrid layer")
     ap.add_argument("--only-allpmult", action="store_true", help="time only the all-PMult layer")
     ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--ablation", action="store_true",
+                    help="also time the layer compiled per-contribution, grouped, grouped+shared (Sec. 6.2)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only copy 4 GiB device-to-device (torch copy kernel) to calibrate HBM counters")
     args = ap.parse_args()
@@ -203,6 +213,25 @@ def main():
                  "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "alg_bytes": ap_bytes,
                  "frac_of_hbm_peak": round(ap_bytes / ap_ms / 1e6 / HBM_PEAK_GBS, 4),
                  "chunks": len(ap_chunks), "speedup_hybrid_vs_allpmult": round(ap_ms / hy_ms, 3)}
+    ablation = None
+    if args.ablation:
+        # the compilations of Sec. 6.2 on the same kernel: every signed term's
+        # factor applied on its own, then grouping, then sharing whole sums,
+        # then sharing partly overlapping sums as well (the default plan)
+        ablation = []
+        for name, flags in (("per-contribution", fiona.FIONA_PLAN_PER_CONTRIBUTION),
+                            ("+grouping", fiona.FIONA_PLAN_NO_SHARING),
+                            ("+sharing", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
+                            ("+partial sharing", 0)):
+            ms, _, _ = time_layer(layer, dev, args.steps, args.warmup, stream, name, flags)
+            c = time_layer.counts
+            ablation.append({"plan": name, "ms_per_step": round(ms, 4),
+                             "value": round(layer.ct_terms / (ms * 1e-3), 1),
+                             "scalar_products": c["n_use"], "pmult": c["pmult_grouped"] - c["n_use"],
+                             "addsub": c["addsub_partial"], "common_terms": c["n_partial"],
+                             "speedup_vs_per_contribution": None})
+        for rec in ablation:
+            rec["speedup_vs_per_contribution"] = round(ablation[0]["ms_per_step"] / rec["ms_per_step"], 3)
     wall = time.perf_counter() - t_wall0
 
     traffic = measured_traffic(cfg.name, "hybrid")
@@ -232,6 +261,7 @@ def main():
                      "kernel": " + ".join(hy_kernels)},
         "all_pmult": allpm,
         "hybrid_chunks": hy_chunks if n_launch > 1 else None,
+        "ablation": ablation,
         "gpu_wall_s": round(wall, 2),
     }
     if not args.no_cpu_baseline:

@@ -84,6 +84,8 @@ void fiona_ctx_destroy(fiona_ctx *ctx);
 #define FIONA_PLAN_HOST_ONLY 2u    /* build and check the plan on the host; upload nothing */
 #define FIONA_PLAN_NO_LDS_SUMS 4u  /* never keep shared signed sums resident in LDS */
 #define FIONA_PLAN_NO_PARTIAL_SHARING 8u   /* share only whole signed sums, no common sub-sums */
+#define FIONA_PLAN_PER_CONTRIBUTION 16u    /* no grouping: a scalar product per nonzero signed term
+                                              (the first compilation of Sec. 6.2; implies NO_SHARING) */
 
 /*
  * One routed layer, in the raw per-(output, term) form the offline compiler

@@ -26,6 +26,7 @@ FIONA_PLAN_NO_SHARING = 1
 FIONA_PLAN_HOST_ONLY = 2
 FIONA_PLAN_NO_LDS_SUMS = 4
 FIONA_PLAN_NO_PARTIAL_SHARING = 8
+FIONA_PLAN_PER_CONTRIBUTION = 16
 
 STATUS = {0: "FIONA_OK", -1: "FIONA_ERR_ARG", -2: "FIONA_ERR_PLAN", -3: "FIONA_ERR_UNSUPPORTED",
           -4: "FIONA_ERR_ALIGN", -5: "FIONA_ERR_ALIAS", -6: "FIONA_ERR_HIP", -7: "FIONA_ERR_NOMEM",

@@ -258,8 +258,12 @@ void find_partial_sums(std::vector<SumBuild> &sums, const std::vector<uint64_t> 
 }
 
 int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
-  const bool share = !(d->flags & FIONA_PLAN_NO_SHARING);
+  // Per-contribution compilation applies every signed term's factor on its
+  // own: each nonzero member is a sum of one member, nothing is shared.
+  const bool per_contribution = (d->flags & FIONA_PLAN_PER_CONTRIBUTION) != 0;
+  const bool share = !(d->flags & FIONA_PLAN_NO_SHARING) && !per_contribution;
   const bool partial = share && !(d->flags & FIONA_PLAN_NO_PARTIAL_SHARING);
+  const size_t part_members = per_contribution ? 1 : fiona::kMaxMembers;
   const uint32_t n_pm = d->pm_off[d->n_out];
   const uint32_t n_group = d->grp_off[d->n_out];
   P->n_member_desc = n_group ? d->grp_mem_off[n_group] : 0;
@@ -279,8 +283,8 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
         nz.push_back({(uint64_t)d->mem_input[m] * 2 + (d->mem_sign[m] < 0 ? 1 : 0), m});
       }
       nz_members += nz.size();
-      for (size_t c0 = 0; c0 < nz.size(); c0 += fiona::kMaxMembers) {
-        const size_t c1 = std::min(nz.size(), c0 + (size_t)fiona::kMaxMembers);
+      for (size_t c0 = 0; c0 < nz.size(); c0 += part_members) {
+        const size_t c1 = std::min(nz.size(), c0 + part_members);
         std::vector<std::pair<uint64_t, uint32_t>> part(nz.begin() + c0, nz.begin() + c1);
         std::sort(part.begin(), part.end());
         const bool flip = (part[0].first & 1) != 0;   // canonical form: first member positive

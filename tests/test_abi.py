@@ -214,3 +214,21 @@ def test_partial_sharing_worked_pair():
     assert st["n_sum_distinct"] == 3 and st["n_partial"] >= 1
     # the three distinct sums need 2 + 2 + 3 Add/Sub; with A0 - A1 shared: 1 + 1 + 1 + 2 (+ 1 to form it)
     assert st["addsub_shared"] == 7 and st["addsub_partial"] <= 5
+
+
+@pytest.mark.parametrize("name", ["vgg11", "bert_ffn"])
+def test_ablation_plans(name):
+    """Sec. 6.2 compilations on one layer: per-contribution applies a scalar
+    product per nonzero signed term; grouping applies one per group (sub-sum);
+    sharing and partial sharing only lower the Add/Sub count."""
+    lay = synth.make_layer(synth.CONFIGS[name], 1)
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    pc = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_PER_CONTRIBUTION).stats()
+    gr = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_NO_SHARING).stats()
+    sh = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_NO_PARTIAL_SHARING).stats()
+    pa = fiona.Plan.from_layer(ctx, lay, flags=HOST).stats()
+    assert pc["n_use"] == pc["n_member_nonzero"] == pc["n_sum_distinct"]
+    assert pc["pmult_grouped"] == pc["pmult_per_contribution"] and pc["addsub_partial"] == 0 and pc["n_partial"] == 0
+    assert gr["n_use"] == sh["n_use"] == pa["n_use"] == lay.n_group   # no group here exceeds 48 members
+    assert gr["pmult_grouped"] == lay.n_pm + lay.n_group < pc["pmult_grouped"]
+    assert gr["addsub_partial"] == gr["addsub_unshared"] >= sh["addsub_partial"] >= pa["addsub_partial"]

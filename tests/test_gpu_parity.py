@@ -118,7 +118,9 @@ def test_small_layer_elementwise(dev, name):
                                         ("ragged_pool", fiona.FIONA_PLAN_NO_LDS_SUMS),
                                         ("ragged_pool", fiona.FIONA_PLAN_NO_SHARING | fiona.FIONA_PLAN_NO_LDS_SUMS),
                                         ("partial_share", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
-                                        ("partial_share", fiona.FIONA_PLAN_NO_LDS_SUMS)])
+                                        ("partial_share", fiona.FIONA_PLAN_NO_LDS_SUMS),
+                                        ("ragged_pool", fiona.FIONA_PLAN_PER_CONTRIBUTION),
+                                        ("partial_share", fiona.FIONA_PLAN_PER_CONTRIBUTION)])
 def test_plan_variants_agree(dev, name, flags):
     layer = _small_layer(name)
     x, pt = synth.input_values(layer), synth.pt_values(layer)
