@@ -31,6 +31,10 @@ constexpr double kCostMember = 0.25;
 constexpr double kCostFinish = 6.0;
 constexpr double kCostChunk = 3.0;
 constexpr double kMinSegmentCost = 128.0;
+// LDS residency and common partial sums must save at least this share of a
+// tile's estimated work, else the plan keeps neither (each costs LDS rows, a
+// barrier and a pass over its sums per tile).
+constexpr double kMinShareGain = 0.02;
 
 LimbConst make_limb_const(uint64_t q) {
   LimbConst c;
@@ -321,6 +325,13 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
                    [&](uint32_t a, uint32_t b) { return sums[a].n_use > sums[b].n_use; });
   const uint32_t lds_free = kMaxInputs - d->n_in - 1;   // slots left after the inputs and the zero row
   if (cand.size() > lds_free) cand.resize(lds_free);
+  // estimated work of a tile without residency or common terms (cost units of
+  // the work-item balance below), and what residency would save
+  double tile_work = (double)n_pm;
+  for (const auto &sb : sums)
+    tile_work += sb.n_use * (kCostUseInline + kCostMember * (double)sb.members.size());
+  double res_gain = 0;
+  for (uint32_t s : cand) res_gain += (sums[s].n_use - 1) * kCostMember * (double)sums[s].members.size();
   std::vector<char> resident(sums.size(), 0);
   for (uint32_t s : cand) resident[s] = 1;
 
@@ -329,12 +340,26 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   // An image of at most half the LDS lets two workgroups share a CU; common
   // terms do not push an image that fits past that line.
   std::vector<PartialBuild> parts;
+  std::vector<std::vector<MemberRef>> members_before;   // restored if the sharing is not kept
+  for (const auto &sb : sums) members_before.push_back(sb.members);
+  double part_gain = 0;
   if (partial && lds_free > cand.size()) {
     std::vector<uint64_t> weight(sums.size());
     for (uint32_t s = 0; s < sums.size(); ++s) weight[s] = resident[s] ? 1 : sums[s].n_use;
     const uint32_t base_rows = d->n_in + 1 + (uint32_t)cand.size();
     const uint32_t cap = base_rows * 2 <= kMaxInputs ? kMaxInputs / 2 : kMaxInputs;
     if (cap > base_rows) find_partial_sums(sums, weight, d->n_in, cap - base_rows, parts);
+    double saved = -2.0 * (double)parts.size();   // each common pair is formed once per tile
+    for (uint32_t s = 0; s < sums.size(); ++s)
+      saved += (double)weight[s] * ((double)members_before[s].size() - (double)sums[s].members.size());
+    part_gain = kCostMember * saved;
+  }
+  if (res_gain + part_gain < kMinShareGain * tile_work) {
+    // not worth its LDS rows and barriers: every signed sum is formed in place
+    for (uint32_t s = 0; s < sums.size(); ++s) sums[s].members = members_before[s];
+    parts.clear();
+    for (uint32_t s : cand) resident[s] = 0;
+    cand.clear();
   }
   const uint32_t n_part = (uint32_t)parts.size();
   uint64_t addsub_partial = n_part;   // one Add/Sub forms each common pair

@@ -279,9 +279,11 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
 
   // 3. shared signed sums, formed once per tile
   uint4 *sums = parts + (size_t)S.n_part * kTile;
-  for (uint32_t s = wave; s < S.n_mat; s += NW)
-    sums[s * kTile + lane] = signed_sum(words[(size_t)mats[s] + lane], lds, lane16);
-  __syncthreads();
+  if (S.n_mat) {   // uniform over the workgroup
+    for (uint32_t s = wave; s < S.n_mat; s += NW)
+      sums[s * kTile + lane] = signed_sum(words[(size_t)mats[s] + lane], lds, lane16);
+    __syncthreads();
+  }
 
   // 4. this wavefront's work items; the first records of each item are loaded
   // while the previous item runs
