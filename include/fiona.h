@@ -203,6 +203,46 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
                         const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
                         hipStream_t stream);
 
+/*
+ * Rescale epilogue: divide ciphertexts by the last modulus q_t = q_{L-1} of the
+ * chain, with rounding, and drop that limb (CKKS rescaling, paper Sec. 2
+ * "Levels and Bootstrapping").  Sec. 4.2 "Combining the Signed and Raw
+ * Routes" rescales an output once, after its routes are summed: this is the
+ * call that follows fiona_hybrid_linear.  Per coefficient, with C the integer
+ * of the L residues: C' = round(C / q_t), kept as residues of the first L-1
+ * moduli.
+ *
+ * NTT convention of every limb (input and output): a_hat_k = sum_n a_n
+ * psi_l^((2k+1) n) mod q_l, k in natural order, psi_l a primitive 2N-th root
+ * of unity mod q_l.
+ *
+ * fiona_rescaler_create: the NTT twiddle tables of every limb (device) and a
+ * workspace for up to max_ct ciphertexts (2 * max_ct * N * 16 bytes).
+ *   psi     host [L] roots psi_l, or NULL for the default: psi_l =
+ *           x^((q_l - 1) / 2N) for the smallest x >= 2 with psi_l^N = -1
+ * Requires N a power of two in [2^8, 2^17], L >= 2 and every q_l = 1 mod 2N.
+ * The rescaler keeps a reference to ctx (which must outlive it).  Errors:
+ * FIONA_ERR_ARG, FIONA_ERR_UNSUPPORTED (N, L, a modulus or a root),
+ * FIONA_ERR_NOMEM, FIONA_ERR_HIP.
+ */
+typedef struct fiona_rescaler fiona_rescaler;
+int fiona_rescaler_create(const fiona_ctx *ctx, const uint64_t *psi, uint32_t max_ct, fiona_rescaler **out);
+void fiona_rescaler_destroy(fiona_rescaler *rescaler);
+
+/*
+ * fiona_rescale: out = in / q_t with rounding, per ciphertext and polynomial.
+ *   in_cts   device, [n_ct][2][L][N] uint64 canonical residues (NTT domain)
+ *   out_cts  device, [n_ct][2][L-1][N] uint64, overwritten with canonical
+ *            residues; must not overlap in_cts
+ *   n_ct     at most the max_ct of the rescaler
+ * Asynchronous on stream; allocates nothing.  The rescaler's workspace is
+ * shared by its calls: one rescaler must not be used by two streams at the
+ * same time.  Errors (nothing is launched): FIONA_ERR_ARG, FIONA_ERR_ALIGN,
+ * FIONA_ERR_ALIAS, FIONA_ERR_HIP.
+ */
+int fiona_rescale(const fiona_rescaler *rescaler, const uint64_t *in_cts, uint32_t n_ct, uint64_t *out_cts,
+                  hipStream_t stream);
+
 /* Static string naming a status code. */
 const char *fiona_status_string(int status);
 

@@ -199,3 +199,56 @@ def hybrid_linear(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t, stream=None) -
     _check(lib().fiona_hybrid_linear(plan.handle, _dptr(in_t, "in_cts", 8), _dptr(pt_t, "pt_diags", 8),
                                      _dptr(sign_t, "ternary_groups", 1), _dptr(scale_t, "scales", 8),
                                      _dptr(out_t, "out_cts", 8), s), "fiona_hybrid_linear")
+
+
+class Rescaler:
+    """NTT tables and workspace for the rescale epilogue (fiona_rescaler_create)."""
+
+    def __init__(self, ctx: Ctx, max_ct: int, psi=None):
+        L = lib()
+        L.fiona_rescaler_create.restype = ctypes.c_int
+        L.fiona_rescaler_create.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32,
+                                            ctypes.POINTER(ctypes.c_void_p)]
+        L.fiona_rescaler_destroy.restype = None
+        L.fiona_rescaler_destroy.argtypes = [ctypes.c_void_p]
+        L.fiona_rescale.restype = ctypes.c_int
+        L.fiona_rescale.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+        self.ctx = ctx
+        self.max_ct = int(max_ct)
+        roots = None
+        if psi is not None:
+            roots = (ctypes.c_uint64 * ctx.L)(*[int(p) for p in psi])
+        h = ctypes.c_void_p()
+        _check(L.fiona_rescaler_create(ctx.handle, ctypes.cast(roots, ctypes.c_void_p) if roots else None,
+                                       self.max_ct, ctypes.byref(h)), "fiona_rescaler_create")
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib().fiona_rescaler_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def rescale(rescaler: Rescaler, in_t, n_ct: int, out_t, stream=None) -> None:
+    """fiona_rescale on torch device tensors: in [n_ct][2][L][N] -> out [n_ct][2][L-1][N]."""
+    import torch
+
+    N, L = rescaler.ctx.N, rescaler.ctx.L
+    if in_t.numel() < n_ct * 2 * L * N or out_t.numel() < n_ct * 2 * (L - 1) * N:
+        raise ValueError("tensors too small for %d ciphertexts" % n_ct)
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    _check(lib().fiona_rescale(rescaler.handle, _dptr(in_t, "in_cts", 8), int(n_ct), _dptr(out_t, "out_cts", 8), s),
+           "fiona_rescale")

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "fiona.h"
+#include "fiona_ctx.hpp"
 #include "hybrid_kernel.hpp"
 
 using fiona::KShape;
@@ -56,12 +57,6 @@ bool ranges_overlap(const void *a, size_t na, const void *b, size_t nb) {
 }
 
 }  // namespace
-
-struct fiona_ctx {
-  uint32_t N = 0, L = 0;
-  std::vector<uint64_t> q;
-  std::vector<LimbConst> limbs;
-};
 
 struct fiona_plan {
   const fiona_ctx *ctx = nullptr;

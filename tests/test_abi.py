@@ -232,3 +232,26 @@ def test_ablation_plans(name):
     assert gr["n_use"] == sh["n_use"] == pa["n_use"] == lay.n_group   # no group here exceeds 48 members
     assert gr["pmult_grouped"] == lay.n_pm + lay.n_group < pc["pmult_grouped"]
     assert gr["addsub_partial"] == gr["addsub_unshared"] >= sh["addsub_partial"] >= pa["addsub_partial"]
+
+
+def test_rescaler_validation_without_device():
+    L = fiona.lib()
+    L.fiona_rescaler_create.restype = ctypes.c_int
+    L.fiona_rescaler_create.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32,
+                                        ctypes.POINTER(ctypes.c_void_p)]
+    h = ctypes.c_void_p()
+    assert L.fiona_rescaler_create(None, None, 4, ctypes.byref(h)) == -1
+    q3 = synth.ntt_primes(1 << 12, 3)
+    ctx = fiona.Ctx(1 << 12, 3, q3)
+    assert L.fiona_rescaler_create(ctx.handle, None, 0, ctypes.byref(h)) == -1          # no ciphertexts
+    one = fiona.Ctx(1 << 12, 1, q3[:1])
+    assert L.fiona_rescaler_create(one.handle, None, 4, ctypes.byref(h)) == -3          # nothing to drop
+    small = fiona.Ctx(128, 2, synth.ntt_primes(128, 2))
+    assert L.fiona_rescaler_create(small.handle, None, 4, ctypes.byref(h)) == -3        # N below 2^8
+    odd = fiona.Ctx(1 << 12, 2, [q3[0], (1 << 40) + 15])                                 # not 1 mod 2N
+    assert L.fiona_rescaler_create(odd.handle, None, 4, ctypes.byref(h)) == -3
+    bad_psi = (ctypes.c_uint64 * 3)(2, 2, 2)                                             # not 2N-th roots
+    assert L.fiona_rescaler_create(ctx.handle, ctypes.cast(bad_psi, ctypes.c_void_p), 4, ctypes.byref(h)) == -3
+    L.fiona_rescale.restype = ctypes.c_int
+    L.fiona_rescale.argtypes = [ctypes.c_void_p] * 2 + [ctypes.c_uint32] + [ctypes.c_void_p] * 2
+    assert L.fiona_rescale(None, None, 1, None, None) == -1
