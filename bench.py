@@ -121,6 +121,41 @@ def time_layer(layer, dev, steps, warmup, stream, label, flags=0):
     return total_ms, total_bytes, per_chunk
 
 
+def time_rescale(layer, dev, steps, warmup, stream):
+    """Time fiona_rescale on n_out ciphertexts of the layer's shape (device-generated
+    residues), all outputs in one call."""
+    import torch
+    import synth.gpu
+    import paper_2609_35352_amd as fiona
+
+    N, L, n = layer.N, layer.L, layer.n_out
+    ctx = fiona.Ctx(N, L, layer.moduli)
+    r = fiona.Rescaler(ctx, n)
+    in_t = torch.empty(n * 2 * L * N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_cts(layer, in_t, n)
+    out_t = torch.empty(n * 2 * (L - 1) * N, dtype=torch.int64, device=dev)
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        fiona.rescale(r, in_t, n, out_t, stream=stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        fiona.rescale(r, in_t, n, out_t, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    nbytes = 8 * n * 2 * N * (L + (L - 1))
+    logn = N.bit_length() - 1
+    butterflies = n * 2 * L * (N // 2) * logn
+    log("[bench] rescale of %d ciphertexts: %.3f ms, %.1f GB/s algorithmic" % (n, ms, nbytes / ms / 1e6))
+    return {"ciphertexts": n, "ms": round(ms, 4), "ct_per_s": round(n / (ms * 1e-3), 1),
+            "alg_bytes": nbytes, "alg_GBps": round(nbytes / ms / 1e6, 1),
+            "frac_of_hbm_peak": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4),
+            "butterflies_per_s": round(butterflies / (ms * 1e-3), 1),
+            "launches": 2 * L}
+
+
 def cpu_baseline(layer, seconds: float = 10.0):
     """The oracle (test infrastructure, plain C) on a bounded sample of the same layer."""
     import oracle
@@ -155,6 +190,8 @@ def main():
     ap.add_argument("--no-allpmult", action="store_true", help="time only the hybrid layer")
     ap.add_argument("--only-allpmult", action="store_true", help="time only the all-PMult layer")
     ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--rescale", action="store_true",
+                    help="also time the rescale epilogue on the layer's outputs (fiona_rescale)")
     ap.add_argument("--ablation", action="store_true",
                     help="also time the layer compiled per-contribution, grouped, grouped+shared (Sec. 6.2)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -232,6 +269,9 @@ def main():
                              "speedup_vs_per_contribution": None})
         for rec in ablation:
             rec["speedup_vs_per_contribution"] = round(ablation[0]["ms_per_step"] / rec["ms_per_step"], 3)
+    rescale = None
+    if args.rescale:
+        rescale = time_rescale(layer, dev, args.steps, args.warmup, stream)
     wall = time.perf_counter() - t_wall0
 
     traffic = measured_traffic(cfg.name, "hybrid")
@@ -262,6 +302,7 @@ def main():
         "all_pmult": allpm,
         "hybrid_chunks": hy_chunks if n_launch > 1 else None,
         "ablation": ablation,
+        "rescale": rescale,
         "gpu_wall_s": round(wall, 2),
     }
     if not args.no_cpu_baseline:

@@ -7,7 +7,7 @@ import subprocess
 
 import numpy as np
 
-from . import TAG_IN, TAG_PT, Layer
+from . import TAG_CT, TAG_IN, TAG_PT, Layer
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "csrc", "synth_fill.hip")
@@ -58,6 +58,18 @@ def fill_inputs(layer: Layer, t) -> None:
     assert t.is_cuda and t.is_contiguous() and t.element_size() == 8 and t.numel() >= n
     m = _moduli(layer)
     rc = lib().synth_fill_uniform(t.data_ptr(), layer.n_in * 2 * layer.L, layer.L, layer.N, layer.seed, TAG_IN,
+                                  ctypes.cast(m, ctypes.c_void_p), _stream())
+    if rc != 0:
+        raise RuntimeError("synth_fill_uniform failed (%d)" % rc)
+
+
+def fill_cts(layer: Layer, t, n_ct: int) -> None:
+    """t: device tensor of >= n_ct*2*L*N 8-byte elements -> n_ct ciphertexts [n_ct][2][L][N]
+    of uniform residues (generator tag TAG_CT)."""
+    n = n_ct * 2 * layer.L * layer.N
+    assert t.is_cuda and t.is_contiguous() and t.element_size() == 8 and t.numel() >= n
+    m = _moduli(layer)
+    rc = lib().synth_fill_uniform(t.data_ptr(), n_ct * 2 * layer.L, layer.L, layer.N, layer.seed, TAG_CT,
                                   ctypes.cast(m, ctypes.c_void_p), _stream())
     if rc != 0:
         raise RuntimeError("synth_fill_uniform failed (%d)" % rc)
