@@ -15,7 +15,8 @@
 //   pass B: for each k2, a DFT of size N1 over n1, giving output k2 + N2 k1.
 // A workgroup takes kCols columns (pass A) or rows (pass B) at once, so every
 // global access is a run of kCols consecutive words; the DFTs run in LDS
-// (radix 2, input in bit-reversed order, output natural).
+// (radix 2, input in bit-reversed order, output natural), up to four stages
+// at a time in registers.
 //
 // Modular products use Shoup's method with precomputed companions
 // ws = floor(w 2^64 / q) (q < 2^50), giving x w mod q in [0, 2q) before one
@@ -48,26 +49,69 @@ __device__ __forceinline__ uint64_t sub_q(uint64_t a, uint64_t b, uint64_t q) { 
 
 __device__ __forceinline__ uint32_t bit_reverse(uint32_t x, uint32_t bits) { return __brev(x) >> (32 - bits); }
 
-// Radix-2 DFT of size M = 2^logM on kNttCols columns held in LDS (column c at
-// x + c*M, loaded in bit-reversed order); natural order on return.
-// tw[t] = w_M^t for t < M/2.
-__device__ __forceinline__ void lds_dft(uint64_t *x, uint32_t logM, const Tw *__restrict__ tw, uint64_t q) {
-  const uint32_t M = 1u << logM, halfM = M >> 1;
-  const uint32_t nb = kNttCols * halfM;
-  for (uint32_t s = 0; s < logM; ++s) {
-    const uint32_t half = 1u << s;
+// LDS column layout: one padding word after every 16, so that the 16-word
+// groups a thread reads (consecutive words, or words 16 apart) fall into
+// different banks.
+__device__ __forceinline__ uint32_t pidx(uint32_t i) { return i + (i >> 4); }
+__host__ __device__ constexpr uint32_t padded_len(uint32_t m) { return m + m / 16; }
+
+// Stages s0 .. s0+R-1 of the radix-2 DFT for the groups of one 16-word item:
+// a group is the 2^R words base + (u << s0) that these stages combine; the
+// item holds 16 >> R groups, kept in registers across the R stages.
+template <int R>
+__device__ __forceinline__ void dft_item(uint64_t *col, uint32_t logM, uint32_t s0, uint32_t item,
+                                         const Tw *tw, uint64_t q) {
+  constexpr uint32_t S = 1u << R, G = 16u >> R;
+#pragma unroll
+  for (uint32_t g = 0; g < G; ++g) {
+    const uint32_t gi = item * G + g;
+    const uint32_t o = gi & ((1u << s0) - 1);
+    const uint32_t base = ((gi >> s0) << (s0 + R)) + o;
+    uint64_t r[S];
+#pragma unroll
+    for (uint32_t u = 0; u < S; ++u) r[u] = col[pidx(base + (u << s0))];
+#pragma unroll
+    for (uint32_t st = 0; st < (uint32_t)R; ++st) {
+      const uint32_t hh = 1u << st, shift = logM - 1 - (s0 + st);
+#pragma unroll
+      for (uint32_t u0 = 0; u0 < S; ++u0) {
+        if ((u0 & (2 * hh - 1)) >= hh) continue;
+        const uint32_t pos = o + ((u0 & (hh - 1)) << s0);
+        const uint64_t a = r[u0], t = mul_tw(r[u0 + hh], tw[pos << shift], q);
+        r[u0] = add_q(a, t, q);
+        r[u0 + hh] = sub_q(a, t, q);
+      }
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < S; ++u) col[pidx(base + (u << s0))] = r[u];
+  }
+}
+
+// Radix-2 DFT of size M = 2^logM (16 <= M <= kNttMaxSide) on kNttCols
+// columns held in LDS (column c at x + c * padded_len(M), loaded in
+// bit-reversed order); natural order on return.  tw[t] = w_M^t for t < M/2
+// (in LDS).  Up to four stages per pass over LDS, in registers.
+__device__ __forceinline__ void lds_dft(uint64_t *x, uint32_t logM, const Tw *tw, uint64_t q) {
+  const uint32_t M = 1u << logM, PM = padded_len(M), per_col = M >> 4;
+  const uint32_t items = kNttCols * per_col;
+  for (uint32_t s0 = 0; s0 < logM; s0 += 4) {
+    const uint32_t R = min(4u, logM - s0);
     __syncthreads();
-    for (uint32_t b = threadIdx.x; b < nb; b += kNttThreads) {
-      const uint32_t c = b >> (logM - 1), j = b & (halfM - 1);
-      const uint32_t pos = j & (half - 1);
-      const uint32_t i0 = ((j >> s) << (s + 1)) | pos, i1 = i0 + half;
-      uint64_t *col = x + c * M;
-      const uint64_t u = col[i0], t = mul_tw(col[i1], tw[pos << (logM - 1 - s)], q);
-      col[i0] = add_q(u, t, q);
-      col[i1] = sub_q(u, t, q);
+    for (uint32_t it = threadIdx.x; it < items; it += kNttThreads) {
+      uint64_t *col = x + (it / per_col) * PM;
+      const uint32_t item = it % per_col;
+      if (R == 4) dft_item<4>(col, logM, s0, item, tw, q);
+      else if (R == 3) dft_item<3>(col, logM, s0, item, tw, q);
+      else if (R == 2) dft_item<2>(col, logM, s0, item, tw, q);
+      else dft_item<1>(col, logM, s0, item, tw, q);
     }
   }
   __syncthreads();
+}
+
+// Copy the M/2 twiddles of the size-M DFT into LDS.
+__device__ __forceinline__ void stage_twiddles(Tw *dst, const Tw *__restrict__ src, uint32_t logM) {
+  for (uint32_t i = threadIdx.x; i < (1u << logM) / 2; i += kNttThreads) dst[i] = src[i];
 }
 
 // What a pass does with the values it loads (pass A) or stores (pass B).
@@ -99,8 +143,10 @@ struct NttPass {
 
 // Pass A: grid (N1 / kNttCols, vectors).
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
-  extern __shared__ uint64_t xs[];   // [kNttCols][N2]
-  const uint32_t N1 = 1u << P.log_n1, N2 = 1u << P.log_n2;
+  extern __shared__ uint64_t xs[];   // [kNttCols][padded N2], then the N2/2 DFT twiddles
+  const uint32_t N1 = 1u << P.log_n1, N2 = 1u << P.log_n2, PM = padded_len(N2);
+  Tw *tw = (Tw *)(xs + kNttCols * PM);
+  stage_twiddles(tw, P.dft_a, P.log_n2);
   const uint32_t c0 = blockIdx.x * kNttCols;
   const uint64_t v = blockIdx.y;
   const uint64_t *in = P.in + v * P.in_stride;
@@ -115,35 +161,37 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
       if (neg) x = sub_q(x, P.q_src_mod_q, P.q);
     }
     if (P.pre) x = mul_tw(x, P.pre[n], P.q);
-    xs[c * N2 + bit_reverse(n2, P.log_n2)] = x;
+    xs[c * PM + pidx(bit_reverse(n2, P.log_n2))] = x;
   }
-  lds_dft(xs, P.log_n2, P.dft_a, P.q);
+  lds_dft(xs, P.log_n2, tw, P.q);
   uint64_t *tmp = P.tmp + v * ((uint64_t)N1 * N2);
   for (uint32_t idx = threadIdx.x; idx < kNttCols * N2; idx += kNttThreads) {
     const uint32_t c = idx & (kNttCols - 1), k2 = idx / kNttCols;
     const uint32_t n1 = c0 + c;
-    tmp[k2 * N1 + n1] = mul_tw(xs[c * N2 + k2], P.mid[n1 * N2 + k2], P.q);
+    tmp[k2 * N1 + n1] = mul_tw(xs[c * PM + pidx(k2)], P.mid[n1 * N2 + k2], P.q);
   }
 }
 
 // Pass B: grid (N2 / kNttCols, vectors).
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
-  extern __shared__ uint64_t xs[];   // [kNttCols][N1]
-  const uint32_t N1 = 1u << P.log_n1, N2 = 1u << P.log_n2;
+  extern __shared__ uint64_t xs[];   // [kNttCols][padded N1], then the N1/2 DFT twiddles
+  const uint32_t N1 = 1u << P.log_n1, N2 = 1u << P.log_n2, PM = padded_len(N1);
+  Tw *tw = (Tw *)(xs + kNttCols * PM);
+  stage_twiddles(tw, P.dft_b, P.log_n1);
   const uint32_t r0 = blockIdx.x * kNttCols;
   const uint64_t v = blockIdx.y;
   const uint64_t *tmp = P.tmp + v * ((uint64_t)N1 * N2);
   for (uint32_t idx = threadIdx.x; idx < kNttCols * N1; idx += kNttThreads) {
     const uint32_t c = idx / N1, n1 = idx & (N1 - 1);
-    xs[c * N1 + bit_reverse(n1, P.log_n1)] = tmp[(r0 + c) * N1 + n1];
+    xs[c * PM + pidx(bit_reverse(n1, P.log_n1))] = tmp[(r0 + c) * N1 + n1];
   }
-  lds_dft(xs, P.log_n1, P.dft_b, P.q);
+  lds_dft(xs, P.log_n1, tw, P.q);
   uint64_t *out = P.out + v * P.out_stride;
   const uint64_t *base = P.base ? P.base + v * P.base_stride : nullptr;
   for (uint32_t idx = threadIdx.x; idx < kNttCols * N1; idx += kNttThreads) {
     const uint32_t c = idx & (kNttCols - 1), k1 = idx / kNttCols;
     const uint32_t k = r0 + c + N2 * k1;
-    uint64_t y = xs[c * N1 + k1];
+    uint64_t y = xs[c * PM + pidx(k1)];
     if (P.post) y = mul_tw(y, P.post[k], P.q);
     if (P.store == kStoreRescale) y = mul_tw(sub_q(base[k], y, P.q), P.inv, P.q);
     out[k] = y;

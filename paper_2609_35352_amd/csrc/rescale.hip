@@ -172,7 +172,8 @@ int fiona_rescaler_create(const fiona_ctx *ctx, const uint64_t *psi, uint32_t ma
       R->inv_qt.push_back(make_tw(powmod_h(qt % q, q - 2, q), q));
       R->qt_mod.push_back(qt % q);
     }
-    const int smem = (int)(fiona::kNttCols * (1u << R->log_n1) * sizeof(uint64_t));
+    const int smem = (int)(fiona::kNttCols * fiona::padded_len(1u << R->log_n1) * sizeof(uint64_t) +
+                           (1u << R->log_n1) / 2 * sizeof(Tw));
     if (hipFuncSetAttribute((const void *)fiona::ntt_pass_a, hipFuncAttributeMaxDynamicSharedMemorySize, smem) !=
             hipSuccess ||
         hipFuncSetAttribute((const void *)fiona::ntt_pass_b, hipFuncAttributeMaxDynamicSharedMemorySize, smem) !=
@@ -207,7 +208,8 @@ int fiona_rescale(const fiona_rescaler *R, const uint64_t *in_cts, uint32_t n_ct
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != R->device) return FIONA_ERR_ARG;
   const uint32_t V = 2 * n_ct, N1 = 1u << R->log_n1, N2 = 1u << R->log_n2;
-  const size_t smem_a = fiona::kNttCols * N2 * sizeof(uint64_t), smem_b = fiona::kNttCols * N1 * sizeof(uint64_t);
+  const size_t smem_a = fiona::kNttCols * fiona::padded_len(N2) * sizeof(uint64_t) + N2 / 2 * sizeof(Tw);
+  const size_t smem_b = fiona::kNttCols * fiona::padded_len(N1) * sizeof(uint64_t) + N1 / 2 * sizeof(Tw);
   const dim3 grid_a(N1 / fiona::kNttCols, V), grid_b(N2 / fiona::kNttCols, V), block(fiona::kNttThreads);
 
   // 1. the last limb back to its coefficients (residues mod q_t, natural order)
