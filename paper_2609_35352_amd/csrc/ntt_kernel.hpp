@@ -18,14 +18,20 @@
 // (radix 2, input in bit-reversed order, output natural), up to four stages
 // at a time in registers.
 //
-// Modular products use Shoup's method with precomputed companions
-// ws = floor(w 2^64 / q) (q < 2^50), giving x w mod q in [0, 2q) before one
-// correction.
+// Arithmetic is in fp64, on exact integers (q < 2^50): a double holds any
+// integer below 2^53, and gfx950 issues fp64 FMA at full rate where 32-bit
+// integer multiplies run at quarter rate.  A modular product b * w follows the
+// FMA method of van der Hoeven, Lecerf and Quintin ("Modular SIMD arithmetic in
+// Mathemagix", 2016): h = fl(b w) and its exact error l = b w - h (one FMA);
+// the quotient k = rint(b * w/q) from one FMA against a rounding constant;
+// then b w - k q = (h - k q) + l exactly.  For |b| < 2^51 and 0 <= w < q the
+// result r satisfies r = b w (mod q) and |r| <= q (1/2 + |b| 2^-54).  Values
+// between stages are signed and lazily reduced; reduce() brings any |x| < 2^52
+// to the exact centred residue, |x| <= (q-1)/2 (the FMA's error |x/q| 2^-53 is
+// below 1/(2q), the distance from x/q to the nearest half-integer).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
-
-#include "modarith.hpp"
 
 namespace fiona {
 
@@ -33,41 +39,69 @@ constexpr uint32_t kNttCols = 16;      // columns (pass A) or rows (pass B) per 
 constexpr uint32_t kNttThreads = 256;
 constexpr uint32_t kNttMaxSide = 512;  // N1, N2 <= 512: N <= 2^17
 
-struct Tw {   // a twiddle and its Shoup companion
-  uint64_t w, ws;
+struct Tw {   // a twiddle w, an integer in [0, q), and fl(w / q)
+  double w, wq;
 };
 
-__device__ __forceinline__ uint64_t mul_tw(uint64_t x, const Tw &t, uint64_t q) {
-  const uint64_t r = x * t.w - __umul64hi(x, t.ws) * q;   // in [0, 2q) for x < 2^64
-  return r >= q ? r - q : r;
+// 1.5 * 2^52: adding it to |v| < 2^51 rounds v to the nearest integer.
+constexpr double kRound = 6755399441055744.0;
+
+__device__ __forceinline__ double mul_tw(double b, const Tw &t, double q) {
+#pragma clang fp contract(off)
+  const double h = b * t.w;
+  const double l = __builtin_fma(b, t.w, -h);
+  const double k = __builtin_fma(b, t.wq, kRound) - kRound;
+  return __builtin_fma(-k, q, h) + l;
 }
-__device__ __forceinline__ uint64_t add_q(uint64_t a, uint64_t b, uint64_t q) {
-  const uint64_t s = a + b;
-  return s >= q ? s - q : s;
+
+__device__ __forceinline__ double reduce(double x, double q, double qinv) {
+#pragma clang fp contract(off)
+  const double k = __builtin_fma(x, qinv, kRound) - kRound;
+  return __builtin_fma(-k, q, x);
 }
-__device__ __forceinline__ uint64_t sub_q(uint64_t a, uint64_t b, uint64_t q) { return a >= b ? a - b : a + q - b; }
+
+// x an integer, |x| < 2^52 -> its residue in [0, q)
+__device__ __forceinline__ double canonical(double x, double q, double qinv) {
+  const double z = reduce(x, q, qinv);
+  return z < 0.0 ? z + q : z;
+}
+
+__device__ __forceinline__ double to_f64(uint64_t x) {   // x < 2^53
+  return __builtin_fma((double)(uint32_t)(x >> 32), 4294967296.0, (double)(uint32_t)x);
+}
+__device__ __forceinline__ uint64_t to_u64(double y) {   // y an integer in [0, 2^53)
+  const uint32_t hi = (uint32_t)(y * 0x1p-32);
+  const uint32_t lo = (uint32_t)__builtin_fma(-(double)hi, 4294967296.0, y);
+  return ((uint64_t)hi << 32) | lo;
+}
 
 __device__ __forceinline__ uint32_t bit_reverse(uint32_t x, uint32_t bits) { return __brev(x) >> (32 - bits); }
 
-// LDS column layout: one padding word after every 16, so that the 16-word
-// groups a thread reads (consecutive words, or words 16 apart) fall into
-// different banks.
+// LDS layout of the kNttCols columns.  The 16 lanes of a quarter wave work on
+// the same word of 16 different columns (the DFT's twiddle reads are then
+// broadcasts), so the column stride is odd: those lanes fall into 16
+// different banks.  Within a column one padding word follows every 16, so
+// that 16 consecutive bit-reversed positions (the row loads of pass B) fall
+// into different banks too.
 __device__ __forceinline__ uint32_t pidx(uint32_t i) { return i + (i >> 4); }
-__host__ __device__ constexpr uint32_t padded_len(uint32_t m) { return m + m / 16; }
+__host__ __device__ constexpr uint32_t padded_len(uint32_t m) { return m + m / 16 + 1; }
 
 // Stages s0 .. s0+R-1 of the radix-2 DFT for the groups of one 16-word item:
 // a group is the 2^R words base + (u << s0) that these stages combine; the
 // item holds 16 >> R groups, kept in registers across the R stages.
+// Entries are |x| <= 0.57 q; every second stage and the last one end with a
+// reduction, so a product's input stays below 1.1 q and every value below
+// 1.7 q; the item leaves |x| <= q/2 behind.
 template <int R>
-__device__ __forceinline__ void dft_item(uint64_t *col, uint32_t logM, uint32_t s0, uint32_t item,
-                                         const Tw *tw, uint64_t q) {
+__device__ __forceinline__ void dft_item(double *col, uint32_t logM, uint32_t s0, uint32_t item, const Tw *tw,
+                                         double q, double qinv) {
   constexpr uint32_t S = 1u << R, G = 16u >> R;
 #pragma unroll
   for (uint32_t g = 0; g < G; ++g) {
     const uint32_t gi = item * G + g;
     const uint32_t o = gi & ((1u << s0) - 1);
     const uint32_t base = ((gi >> s0) << (s0 + R)) + o;
-    uint64_t r[S];
+    double r[S];
 #pragma unroll
     for (uint32_t u = 0; u < S; ++u) r[u] = col[pidx(base + (u << s0))];
 #pragma unroll
@@ -77,9 +111,13 @@ __device__ __forceinline__ void dft_item(uint64_t *col, uint32_t logM, uint32_t 
       for (uint32_t u0 = 0; u0 < S; ++u0) {
         if ((u0 & (2 * hh - 1)) >= hh) continue;
         const uint32_t pos = o + ((u0 & (hh - 1)) << s0);
-        const uint64_t a = r[u0], t = mul_tw(r[u0 + hh], tw[pos << shift], q);
-        r[u0] = add_q(a, t, q);
-        r[u0 + hh] = sub_q(a, t, q);
+        const double a = r[u0], t = mul_tw(r[u0 + hh], tw[pos << shift], q);
+        r[u0] = a + t;
+        r[u0 + hh] = a - t;
+      }
+      if ((st & 1) || st + 1 == (uint32_t)R) {
+#pragma unroll
+        for (uint32_t u = 0; u < S; ++u) r[u] = reduce(r[u], q, qinv);
       }
     }
 #pragma unroll
@@ -87,23 +125,25 @@ __device__ __forceinline__ void dft_item(uint64_t *col, uint32_t logM, uint32_t 
   }
 }
 
-// Radix-2 DFT of size M = 2^logM (16 <= M <= kNttMaxSide) on kNttCols
+// Radix-2 DFT of size M = 2^LOGM (16 <= M <= kNttMaxSide) on kNttCols
 // columns held in LDS (column c at x + c * padded_len(M), loaded in
-// bit-reversed order); natural order on return.  tw[t] = w_M^t for t < M/2
-// (in LDS).  Up to four stages per pass over LDS, in registers.
-__device__ __forceinline__ void lds_dft(uint64_t *x, uint32_t logM, const Tw *tw, uint64_t q) {
-  const uint32_t M = 1u << logM, PM = padded_len(M), per_col = M >> 4;
-  const uint32_t items = kNttCols * per_col;
-  for (uint32_t s0 = 0; s0 < logM; s0 += 4) {
-    const uint32_t R = min(4u, logM - s0);
+// bit-reversed order, entries |x| <= 0.57 q); natural order on return, each
+// entry the centred residue.  tw[t] = w_M^t for t < M/2 (in LDS).  Up to four
+// stages per pass over LDS, in registers; item it works on column
+// it % kNttCols.
+template <uint32_t LOGM>
+__device__ __forceinline__ void lds_dft(double *x, const Tw *tw, double q, double qinv) {
+  constexpr uint32_t M = 1u << LOGM, PM = padded_len(M), items = kNttCols * (M >> 4);
+#pragma unroll
+  for (uint32_t s0 = 0; s0 < LOGM; s0 += 4) {
     __syncthreads();
     for (uint32_t it = threadIdx.x; it < items; it += kNttThreads) {
-      uint64_t *col = x + (it / per_col) * PM;
-      const uint32_t item = it % per_col;
-      if (R == 4) dft_item<4>(col, logM, s0, item, tw, q);
-      else if (R == 3) dft_item<3>(col, logM, s0, item, tw, q);
-      else if (R == 2) dft_item<2>(col, logM, s0, item, tw, q);
-      else dft_item<1>(col, logM, s0, item, tw, q);
+      double *col = x + (it % kNttCols) * PM;
+      const uint32_t item = it / kNttCols;
+      if (LOGM - s0 >= 4) dft_item<4>(col, LOGM, s0, item, tw, q, qinv);
+      else if (LOGM - s0 == 3) dft_item<3>(col, LOGM, s0, item, tw, q, qinv);
+      else if (LOGM - s0 == 2) dft_item<2>(col, LOGM, s0, item, tw, q, qinv);
+      else dft_item<1>(col, LOGM, s0, item, tw, q, qinv);
     }
   }
   __syncthreads();
@@ -114,87 +154,145 @@ __device__ __forceinline__ void stage_twiddles(Tw *dst, const Tw *__restrict__ s
   for (uint32_t i = threadIdx.x; i < (1u << logM) / 2; i += kNttThreads) dst[i] = src[i];
 }
 
-// What a pass does with the values it loads (pass A) or stores (pass B).
+// What a pass reads (pass A) and writes (pass B).
 enum NttLoad : uint32_t {
-  kLoadPlain = 0,    // the input is already a residue mod q
-  kLoadCentred = 1,  // the input is a residue mod q_src: take its centred value mod q
+  kLoadU64 = 0,   // residues in [0, q) as uint64
+  kLoadF64 = 1,   // signed integers as doubles, |x| < 2^49 (a centred residue of another modulus)
 };
 enum NttStore : uint32_t {
-  kStorePlain = 0,    // store the transform
-  kStoreRescale = 1,  // store (base - transform) * inv mod q
+  kStoreU64 = 0,      // the transform, residues in [0, q) as uint64
+  kStoreF64 = 1,      // the transform, centred residues as doubles
+  kStoreRescale = 2,  // (base - transform) * inv mod q, in [0, q) as uint64
 };
 
 struct NttPass {
-  const uint64_t *in;    // pass A: vector v, element n at in + v * in_stride + n
-  uint64_t *tmp;         // the transposed intermediate, vector v at tmp + v * N
-  uint64_t *out;         // pass B: vector v, element k at out + v * out_stride + k
-  const uint64_t *base;  // kStoreRescale: base + v * base_stride + k
+  const void *in;        // pass A: vector v, element n at in + v * in_stride + n
+  double *tmp;           // the transposed intermediate, vector v at tmp + v * N
+  void *out;             // pass B: vector v, element k at out + v * out_stride + k
+  const uint64_t *base;  // kStoreRescale: base + v * base_stride + k, residues in [0, q)
   const Tw *pre;         // pass A: multiply input n by pre[n] (null: by 1)
-  const Tw *mid;         // pass A: mid[n1 N2 + k2]
+  const Tw *mid;         // pass A: mid[k2 N1 + n1] = omega^(n1 k2)
   const Tw *dft_a;       // size-N2 DFT twiddles (N2 / 2)
   const Tw *dft_b;       // size-N1 DFT twiddles (N1 / 2)
   const Tw *post;        // pass B: multiply output k by post[k] (null: by 1)
-  Tw inv;                // kStoreRescale: q_src^-1 mod q
-  uint64_t q, q_src, q_src_mod_q;
-  double qinv;           // 1 / q, for reducing a residue mod q_src
+  Tw inv;                // kStoreRescale: the factor applied after the subtraction
+  double q, qinv;        // the modulus and fl(1 / q)
   uint64_t in_stride, out_stride, base_stride;
   uint32_t log_n1, log_n2, load, store;
 };
 
-// Pass A: grid (N1 / kNttCols, vectors).
+// Global loads and stores go in batches of up to kNttBatch per thread, all
+// issued before the first is used.
+constexpr uint32_t kNttBatch = 16;
+
+// Pass A, N2 = 2^LOGM: grid (N1 / kNttCols, vectors).  Thread t handles
+// column c0 + t % kNttCols, rows n2 = t / kNttCols + j * (kNttThreads / kNttCols).
+template <uint32_t LOGM>
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
-  extern __shared__ uint64_t xs[];   // [kNttCols][padded N2], then the N2/2 DFT twiddles
-  const uint32_t N1 = 1u << P.log_n1, N2 = 1u << P.log_n2, PM = padded_len(N2);
+  constexpr uint32_t M = 1u << LOGM, PM = padded_len(M), PER = kNttCols * M / kNttThreads;
+  constexpr uint32_t B = PER < kNttBatch ? PER : kNttBatch, RSTEP = kNttThreads / kNttCols;
+  extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * PM);
-  stage_twiddles(tw, P.dft_a, P.log_n2);
-  const uint32_t c0 = blockIdx.x * kNttCols;
+  stage_twiddles(tw, P.dft_a, LOGM);
+  const uint32_t N1 = 1u << P.log_n1, c = threadIdx.x % kNttCols, r = threadIdx.x / kNttCols;
+  const uint32_t n1 = blockIdx.x * kNttCols + c;
   const uint64_t v = blockIdx.y;
-  const uint64_t *in = P.in + v * P.in_stride;
-  const uint64_t half_src = P.q_src >> 1;
-  for (uint32_t idx = threadIdx.x; idx < kNttCols * N2; idx += kNttThreads) {
-    const uint32_t c = idx & (kNttCols - 1), n2 = idx / kNttCols;
-    const uint32_t n = c0 + c + N1 * n2;
-    uint64_t x = in[n];
-    if (P.load == kLoadCentred) {   // x in [0, q_src): its centred value mod q
-      const bool neg = x > half_src;
-      x = reduce_small(x, P.q, P.qinv);
-      if (neg) x = sub_q(x, P.q_src_mod_q, P.q);
+  const double q = P.q, qinv = P.qinv;
+#pragma unroll
+  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
+    double x[B];
+    if (P.load == kLoadF64) {
+      const double *in = (const double *)P.in + v * P.in_stride + n1;
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) x[j] = in[(size_t)N1 * (r + (b0 + j) * RSTEP)];
+    } else {
+      const uint64_t *in = (const uint64_t *)P.in + v * P.in_stride + n1;
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) x[j] = to_f64(in[(size_t)N1 * (r + (b0 + j) * RSTEP)]);
     }
-    if (P.pre) x = mul_tw(x, P.pre[n], P.q);
-    xs[c * PM + pidx(bit_reverse(n2, P.log_n2))] = x;
+    if (P.pre) {
+      Tw t[B];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) t[j] = P.pre[n1 + N1 * (r + (b0 + j) * RSTEP)];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) x[j] = mul_tw(x[j], t[j], q);
+    } else {
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) x[j] = reduce(x[j], q, qinv);
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) xs[c * PM + pidx(bit_reverse(r + (b0 + j) * RSTEP, LOGM))] = x[j];
   }
-  lds_dft(xs, P.log_n2, tw, P.q);
-  uint64_t *tmp = P.tmp + v * ((uint64_t)N1 * N2);
-  for (uint32_t idx = threadIdx.x; idx < kNttCols * N2; idx += kNttThreads) {
-    const uint32_t c = idx & (kNttCols - 1), k2 = idx / kNttCols;
-    const uint32_t n1 = c0 + c;
-    tmp[k2 * N1 + n1] = mul_tw(xs[c * PM + pidx(k2)], P.mid[n1 * N2 + k2], P.q);
+  lds_dft<LOGM>(xs, tw, q, qinv);
+  double *tmp = P.tmp + v * ((uint64_t)N1 * M) + n1;
+#pragma unroll
+  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
+    Tw t[B];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) t[j] = P.mid[(size_t)(r + (b0 + j) * RSTEP) * N1 + n1];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) {
+      const uint32_t k2 = r + (b0 + j) * RSTEP;
+      tmp[(size_t)k2 * N1] = mul_tw(xs[c * PM + pidx(k2)], t[j], q);
+    }
   }
 }
 
-// Pass B: grid (N2 / kNttCols, vectors).
+// Pass B, N1 = 2^LOGM: grid (N2 / kNttCols, vectors).  Rows of the
+// intermediate are loaded whole; thread t stores column k2 = r0 + t % kNttCols.
+template <uint32_t LOGM>
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
-  extern __shared__ uint64_t xs[];   // [kNttCols][padded N1], then the N1/2 DFT twiddles
-  const uint32_t N1 = 1u << P.log_n1, N2 = 1u << P.log_n2, PM = padded_len(N1);
+  constexpr uint32_t M = 1u << LOGM, PM = padded_len(M), PER = kNttCols * M / kNttThreads;
+  constexpr uint32_t B = PER < kNttBatch ? PER : kNttBatch, RSTEP = kNttThreads / kNttCols;
+  extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * PM);
-  stage_twiddles(tw, P.dft_b, P.log_n1);
-  const uint32_t r0 = blockIdx.x * kNttCols;
+  stage_twiddles(tw, P.dft_b, LOGM);
+  const uint32_t N2 = 1u << P.log_n2, r0 = blockIdx.x * kNttCols;
   const uint64_t v = blockIdx.y;
-  const uint64_t *tmp = P.tmp + v * ((uint64_t)N1 * N2);
-  for (uint32_t idx = threadIdx.x; idx < kNttCols * N1; idx += kNttThreads) {
-    const uint32_t c = idx / N1, n1 = idx & (N1 - 1);
-    xs[c * PM + pidx(bit_reverse(n1, P.log_n1))] = tmp[(r0 + c) * N1 + n1];
+  const double q = P.q, qinv = P.qinv;
+  const double *tmp = P.tmp + v * ((uint64_t)N2 * M) + (size_t)r0 * M;
+#pragma unroll
+  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
+    double x[B];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) x[j] = tmp[threadIdx.x + (b0 + j) * kNttThreads];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) {
+      const uint32_t idx = threadIdx.x + (b0 + j) * kNttThreads;
+      xs[(idx >> LOGM) * PM + pidx(bit_reverse(idx & (M - 1), LOGM))] = x[j];
+    }
   }
-  lds_dft(xs, P.log_n1, tw, P.q);
-  uint64_t *out = P.out + v * P.out_stride;
-  const uint64_t *base = P.base ? P.base + v * P.base_stride : nullptr;
-  for (uint32_t idx = threadIdx.x; idx < kNttCols * N1; idx += kNttThreads) {
-    const uint32_t c = idx & (kNttCols - 1), k1 = idx / kNttCols;
-    const uint32_t k = r0 + c + N2 * k1;
-    uint64_t y = xs[c * PM + pidx(k1)];
-    if (P.post) y = mul_tw(y, P.post[k], P.q);
-    if (P.store == kStoreRescale) y = mul_tw(sub_q(base[k], y, P.q), P.inv, P.q);
-    out[k] = y;
+  lds_dft<LOGM>(xs, tw, q, qinv);
+  const uint32_t c = threadIdx.x % kNttCols, r = threadIdx.x / kNttCols, k2 = r0 + c;
+#pragma unroll
+  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
+    double y[B];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) y[j] = xs[c * PM + pidx(r + (b0 + j) * RSTEP)];
+    if (P.post) {
+      Tw t[B];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) t[j] = P.post[k2 + (size_t)N2 * (r + (b0 + j) * RSTEP)];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) y[j] = mul_tw(y[j], t[j], q);
+    }
+    if (P.store == kStoreF64) {
+      double *out = (double *)P.out + v * P.out_stride + k2;
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) out[(size_t)N2 * (r + (b0 + j) * RSTEP)] = reduce(y[j], q, qinv);
+    } else {
+      if (P.store == kStoreRescale) {
+        const uint64_t *base = P.base + v * P.base_stride + k2;
+        uint64_t bv[B];
+#pragma unroll
+        for (uint32_t j = 0; j < B; ++j) bv[j] = base[(size_t)N2 * (r + (b0 + j) * RSTEP)];
+#pragma unroll
+        for (uint32_t j = 0; j < B; ++j) y[j] = mul_tw(to_f64(bv[j]) - y[j], P.inv, q);
+      }
+      uint64_t *out = (uint64_t *)P.out + v * P.out_stride + k2;
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) out[(size_t)N2 * (r + (b0 + j) * RSTEP)] = to_u64(canonical(y[j], q, qinv));
+    }
   }
 }
 

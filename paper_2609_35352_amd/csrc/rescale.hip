@@ -37,7 +37,7 @@ uint64_t powmod_h(uint64_t b, uint64_t e, uint64_t q) {
   return r;
 }
 
-Tw make_tw(uint64_t w, uint64_t q) { return Tw{w, (uint64_t)(((unsigned __int128)w << 64) / q)}; }
+Tw make_tw(uint64_t w, uint64_t q) { return Tw{(double)w, (double)w / (double)q}; }
 
 // The default root: psi = x^((q-1)/2N) for the smallest x >= 2 with psi^N = -1.
 uint64_t default_psi(uint32_t N, uint64_t q) {
@@ -48,7 +48,7 @@ uint64_t default_psi(uint32_t N, uint64_t q) {
   return 0;
 }
 
-// Tables of one direction of one limb.  Forward: pre = psi^n, mid = omega^(n1 k2),
+// Tables of one direction of one limb.  Forward: pre = psi^n, mid = omega^(n1 k2) at k2 N1 + n1,
 // DFT roots omega^N1 (size N2) and omega^N2 (size N1).  Inverse: omega -> omega^-1,
 // no pre, post = N^-1 psi^-k.
 struct TableSet {
@@ -73,7 +73,7 @@ TableSet make_tables(uint32_t log_n1, uint32_t log_n2, uint64_t q, uint64_t psi,
   for (uint32_t n1 = 0; n1 < N1; ++n1) {
     const uint64_t step = powmod_h(omega, n1, q);
     uint64_t p = 1;
-    for (uint32_t k2 = 0; k2 < N2; ++k2, p = mulmod_h(p, step, q)) t.mid[(size_t)n1 * N2 + k2] = make_tw(p, q);
+    for (uint32_t k2 = 0; k2 < N2; ++k2, p = mulmod_h(p, step, q)) t.mid[(size_t)k2 * N1 + n1] = make_tw(p, q);
   }
   const uint64_t w2 = powmod_h(omega, N1, q), w1 = powmod_h(omega, N2, q);
   t.dft_a.resize(N2 / 2);
@@ -83,6 +83,34 @@ TableSet make_tables(uint32_t log_n1, uint32_t log_n2, uint64_t q, uint64_t psi,
   p = 1;
   for (uint32_t i = 0; i < N1 / 2; ++i, p = mulmod_h(p, w1, q)) t.dft_b[i] = make_tw(p, q);
   return t;
+}
+
+// The passes are instantiated per DFT side 2^4 .. 2^9.
+template <uint32_t LOG>
+void launch_pair(bool a, dim3 grid, size_t smem, hipStream_t stream, const NttPass &P) {
+  if (a) hipLaunchKernelGGL(fiona::ntt_pass_a<LOG>, grid, dim3(fiona::kNttThreads), smem, stream, P);
+  else hipLaunchKernelGGL(fiona::ntt_pass_b<LOG>, grid, dim3(fiona::kNttThreads), smem, stream, P);
+}
+
+void launch_pass(bool a, uint32_t log_side, dim3 grid, hipStream_t stream, const NttPass &P) {
+  const size_t smem = fiona::kNttCols * fiona::padded_len(1u << log_side) * sizeof(double) +
+                      (1u << log_side) / 2 * sizeof(Tw);
+  switch (log_side) {
+    case 4: launch_pair<4>(a, grid, smem, stream, P); break;
+    case 5: launch_pair<5>(a, grid, smem, stream, P); break;
+    case 6: launch_pair<6>(a, grid, smem, stream, P); break;
+    case 7: launch_pair<7>(a, grid, smem, stream, P); break;
+    case 8: launch_pair<8>(a, grid, smem, stream, P); break;
+    default: launch_pair<9>(a, grid, smem, stream, P); break;
+  }
+}
+
+template <uint32_t LOG>
+bool allow_smem(int bytes) {
+  return hipFuncSetAttribute((const void *)fiona::ntt_pass_a<LOG>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             bytes) == hipSuccess &&
+         hipFuncSetAttribute((const void *)fiona::ntt_pass_b<LOG>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             bytes) == hipSuccess;
 }
 
 struct LimbTables {
@@ -99,8 +127,8 @@ struct fiona_rescaler {
   std::vector<LimbTables> fwd;   // limbs 0 .. L-2
   LimbTables inv;                // limb L-1
   std::vector<Tw> inv_qt;        // q_t^-1 mod q_l
-  std::vector<uint64_t> qt_mod;  // q_t mod q_l
-  uint64_t *W = nullptr, *T = nullptr;
+  double *W = nullptr;           // the centred remainders [INTT_t(in_t)], one vector per polynomial
+  double *T = nullptr;           // the transposed intermediate of the passes
 };
 
 extern "C" {
@@ -143,7 +171,7 @@ int fiona_rescaler_create(const fiona_ctx *ctx, const uint64_t *psi, uint32_t ma
     };
     for (auto &t : sets) offs.push_back(Off{put(t.pre), put(t.mid), put(t.dft_a), put(t.dft_b), put(t.post)});
     const size_t table_bytes = (all.size() * sizeof(Tw) + 255) / 256 * 256;
-    const size_t vec_bytes = (size_t)2 * max_ct * N * sizeof(uint64_t);
+    const size_t vec_bytes = (size_t)2 * max_ct * N * sizeof(double);
     if (hipGetDevice(&R->device) != hipSuccess) {
       delete R;
       return FIONA_ERR_HIP;
@@ -164,20 +192,17 @@ int fiona_rescaler_create(const fiona_ctx *ctx, const uint64_t *psi, uint32_t ma
       if (l + 1 < L) R->fwd.push_back(lt);
       else R->inv = lt;
     }
-    R->W = (uint64_t *)((char *)R->dev + table_bytes);
-    R->T = (uint64_t *)((char *)R->dev + table_bytes + vec_bytes);
+    R->W = (double *)((char *)R->dev + table_bytes);
+    R->T = (double *)((char *)R->dev + table_bytes + vec_bytes);
     const uint64_t qt = ctx->q[L - 1];
     for (uint32_t l = 0; l + 1 < L; ++l) {
       const uint64_t q = ctx->q[l];
       R->inv_qt.push_back(make_tw(powmod_h(qt % q, q - 2, q), q));
-      R->qt_mod.push_back(qt % q);
     }
-    const int smem = (int)(fiona::kNttCols * fiona::padded_len(1u << R->log_n1) * sizeof(uint64_t) +
-                           (1u << R->log_n1) / 2 * sizeof(Tw));
-    if (hipFuncSetAttribute((const void *)fiona::ntt_pass_a, hipFuncAttributeMaxDynamicSharedMemorySize, smem) !=
-            hipSuccess ||
-        hipFuncSetAttribute((const void *)fiona::ntt_pass_b, hipFuncAttributeMaxDynamicSharedMemorySize, smem) !=
-            hipSuccess) {
+    const int smem = (int)(fiona::kNttCols * fiona::padded_len(fiona::kNttMaxSide) * sizeof(double) +
+                           fiona::kNttMaxSide / 2 * sizeof(Tw));
+    if (!allow_smem<4>(smem) || !allow_smem<5>(smem) || !allow_smem<6>(smem) || !allow_smem<7>(smem) ||
+        !allow_smem<8>(smem) || !allow_smem<9>(smem)) {
       fiona_rescaler_destroy(R);
       return FIONA_ERR_HIP;
     }
@@ -208,13 +233,13 @@ int fiona_rescale(const fiona_rescaler *R, const uint64_t *in_cts, uint32_t n_ct
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != R->device) return FIONA_ERR_ARG;
   const uint32_t V = 2 * n_ct, N1 = 1u << R->log_n1, N2 = 1u << R->log_n2;
-  const size_t smem_a = fiona::kNttCols * fiona::padded_len(N2) * sizeof(uint64_t) + N2 / 2 * sizeof(Tw);
-  const size_t smem_b = fiona::kNttCols * fiona::padded_len(N1) * sizeof(uint64_t) + N1 / 2 * sizeof(Tw);
-  const dim3 grid_a(N1 / fiona::kNttCols, V), grid_b(N2 / fiona::kNttCols, V), block(fiona::kNttThreads);
+  const dim3 grid_a(N1 / fiona::kNttCols, V), grid_b(N2 / fiona::kNttCols, V);
 
-  // 1. the last limb back to its coefficients (residues mod q_t, natural order)
+  // 1. the last limb back to its coefficients, kept as centred residues mod q_t
+  const uint64_t qt = R->ctx->q[L - 1];
   NttPass P{};
-  P.q = R->ctx->q[L - 1];
+  P.q = (double)qt;
+  P.qinv = 1.0 / (double)qt;
   P.log_n1 = R->log_n1;
   P.log_n2 = R->log_n2;
   P.in = in_cts + (L - 1) * N;
@@ -226,19 +251,18 @@ int fiona_rescale(const fiona_rescaler *R, const uint64_t *in_cts, uint32_t n_ct
   P.dft_a = R->inv.dft_a;
   P.dft_b = R->inv.dft_b;
   P.post = R->inv.post;
-  P.load = fiona::kLoadPlain;
-  P.store = fiona::kStorePlain;
-  hipLaunchKernelGGL(fiona::ntt_pass_a, grid_a, block, smem_a, stream, P);
-  hipLaunchKernelGGL(fiona::ntt_pass_b, grid_b, block, smem_b, stream, P);
+  P.load = fiona::kLoadU64;
+  P.store = fiona::kStoreF64;
+  launch_pass(true, R->log_n2, grid_a, stream, P);
+  launch_pass(false, R->log_n1, grid_b, stream, P);
 
-  // 2. every other limb: the centred remainder into its NTT domain, subtracted,
-  //    multiplied by q_t^-1
+  // 2. every other limb: the centred remainder (a signed integer, so its
+  //    residue mod q_l comes with the first product) into its NTT domain,
+  //    subtracted, multiplied by q_t^-1
   for (uint32_t l = 0; l + 1 < L; ++l) {
     NttPass Q{};
-    Q.q = R->ctx->q[l];
-    Q.qinv = R->ctx->limbs[l].qinv;
-    Q.q_src = R->ctx->q[L - 1];
-    Q.q_src_mod_q = R->qt_mod[l];
+    Q.q = (double)R->ctx->q[l];
+    Q.qinv = 1.0 / (double)R->ctx->q[l];
     Q.log_n1 = R->log_n1;
     Q.log_n2 = R->log_n2;
     Q.in = R->W;
@@ -253,10 +277,10 @@ int fiona_rescale(const fiona_rescaler *R, const uint64_t *in_cts, uint32_t n_ct
     Q.dft_a = R->fwd[l].dft_a;
     Q.dft_b = R->fwd[l].dft_b;
     Q.inv = R->inv_qt[l];
-    Q.load = fiona::kLoadCentred;
+    Q.load = fiona::kLoadF64;
     Q.store = fiona::kStoreRescale;
-    hipLaunchKernelGGL(fiona::ntt_pass_a, grid_a, block, smem_a, stream, Q);
-    hipLaunchKernelGGL(fiona::ntt_pass_b, grid_b, block, smem_b, stream, Q);
+    launch_pass(true, R->log_n2, grid_a, stream, Q);
+    launch_pass(false, R->log_n1, grid_b, stream, Q);
   }
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   return FIONA_OK;
