@@ -57,7 +57,7 @@ def measured_traffic(workload: str, variant: str):
     return None if v is None else float(v["bytes_per_launch"])
 
 
-def time_layer(layer, dev, steps, warmup, stream, label, flags=0):
+def time_layer(layer, dev, steps, warmup, stream, label, flags=0, padded=True):
     """Run every output chunk of `layer` with plans made under `flags`; return
     (sum of per-chunk ms per launch, algorithmic bytes, per-chunk records).
     time_layer.kernels names the kernel instances and time_layer.counts sums
@@ -74,9 +74,16 @@ def time_layer(layer, dev, steps, warmup, stream, label, flags=0):
     in_t = torch.empty(layer.n_in * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
     synth.gpu.fill_inputs(layer, in_t)
     subs = [synth.chunk_layer(layer, a, b) for a, b in chunks]
+    # plaintext rows at the library's padded pitch (or packed, pitch L*N)
+    if padded is True:
+        pitch = ctx.pt_pitch_hint()
+    elif padded is False:
+        pitch = layer.L * layer.N
+    else:   # an explicit pad in words
+        pitch = layer.L * layer.N + int(padded)
     max_pt = max(max(1, s.n_pt) for s in subs)
     max_out = max(s.n_out for s in subs)
-    pt_t = torch.empty(max_pt * layer.L * layer.N, dtype=torch.int64, device=dev)
+    pt_t = torch.empty((max_pt - 1) * pitch + layer.L * layer.N, dtype=torch.int64, device=dev)
     out_t = torch.empty(max_out * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
     total_ms = 0.0
     total_bytes = 0
@@ -84,8 +91,8 @@ def time_layer(layer, dev, steps, warmup, stream, label, flags=0):
     waves = set()
     counts = {}
     for ci, sub in enumerate(subs):
-        synth.gpu.fill_pts(sub, pt_t)
-        plan = fiona.Plan.from_layer(ctx, sub, flags=flags)
+        synth.gpu.fill_pts(sub, pt_t, pitch)
+        plan = fiona.Plan.from_layer(ctx, sub, flags=flags, pt_pitch=pitch)
         sign_t = torch.from_numpy(np.ascontiguousarray(sub.mem_sign)).to(dev) if sub.mem_sign.size else \
             torch.zeros(1, dtype=torch.int8, device=dev)
         scale_t = torch.from_numpy(np.ascontiguousarray(sub.scales.view(np.int64))).to(dev) if sub.scales.size \
@@ -117,6 +124,7 @@ def time_layer(layer, dev, steps, warmup, stream, label, flags=0):
     del pt_t, out_t, in_t
     torch.cuda.empty_cache()
     time_layer.kernels = ["hybrid_linear_kernel<%d>" % w for w in sorted(waves)]
+    time_layer.pitch = pitch
     time_layer.counts = counts
     return total_ms, total_bytes, per_chunk
 
@@ -194,6 +202,10 @@ def main():
                     help="also time the rescale epilogue on the layer's outputs (fiona_rescale)")
     ap.add_argument("--ablation", action="store_true",
                     help="also time the layer compiled per-contribution, grouped, grouped+shared (Sec. 6.2)")
+    ap.add_argument("--packed-pts", action="store_true",
+                    help="plaintext rows packed at pitch L*N instead of the library's padded pitch hint")
+    ap.add_argument("--pt-pad", type=int, default=None,
+                    help="plaintext pitch L*N + PT_PAD words (overrides the pitch hint)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only copy 4 GiB device-to-device (torch copy kernel) to calibrate HBM counters")
     args = ap.parse_args()
@@ -225,19 +237,23 @@ def main():
     stream = torch.cuda.Stream(device=dev)   # default priority
     cfg = synth.CONFIGS[args.config]
     layer = synth.make_layer(cfg, args.seed)
+    pad_mode = False if args.packed_pts else (True if args.pt_pad is None else args.pt_pad)
     log("[bench] %s: %s" % (cfg.name, cfg.description))
 
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
     if args.only_allpmult:
         apl = synth.all_pmult_layer(layer)
-        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult")
+        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult",
+                                                padded=pad_mode)
         print(json.dumps({"variant": "all-PMult", "workload": cfg.name, "ms_per_step": round(ap_ms, 4),
                           "value": round(layer.ct_terms / (ap_ms * 1e-3), 1), "unit": "ct-terms/s",
                           "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "chunks": ap_chunks}), flush=True)
         return
-    hy_ms, hy_bytes, hy_chunks = time_layer(layer, dev, args.steps, args.warmup, stream, "hybrid")
+    hy_ms, hy_bytes, hy_chunks = time_layer(layer, dev, args.steps, args.warmup, stream, "hybrid",
+                                            padded=pad_mode)
     hy_kernels = time_layer.kernels
+    hy_pitch = time_layer.pitch
     torch.cuda.synchronize()
     hy_value = layer.ct_terms / (hy_ms * 1e-3)
     hy_gbs = hy_bytes / hy_ms / 1e6
@@ -245,7 +261,8 @@ def main():
     allpm = None
     if not args.no_allpmult:
         apl = synth.all_pmult_layer(layer)
-        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult")
+        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult",
+                                                padded=pad_mode)
         allpm = {"value": round(layer.ct_terms / (ap_ms * 1e-3), 1), "ms_per_step": round(ap_ms, 4),
                  "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "alg_bytes": ap_bytes,
                  "frac_of_hbm_peak": round(ap_bytes / ap_ms / 1e6 / HBM_PEAK_GBS, 4),
@@ -260,7 +277,8 @@ def main():
                             ("+grouping", fiona.FIONA_PLAN_NO_SHARING),
                             ("+sharing", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
                             ("+partial sharing", 0)):
-            ms, _, _ = time_layer(layer, dev, args.steps, args.warmup, stream, name, flags)
+            ms, _, _ = time_layer(layer, dev, args.steps, args.warmup, stream, name, flags,
+                                  padded=pad_mode)
             c = time_layer.counts
             ablation.append({"plan": name, "ms_per_step": round(ms, 4),
                              "value": round(layer.ct_terms / (ms * 1e-3), 1),
@@ -292,7 +310,8 @@ def main():
         "config": {"workload": "%s: %s" % (cfg.name, cfg.description), "N": cfg.N, "L": cfg.L,
                    "n_in": cfg.n_in, "n_out": cfg.n_out, "terms_per_output": cfg.T, "group": cfg.g,
                    "ternary_groups": layer.n_group, "raw_terms": layer.n_pm, "ct_terms": layer.ct_terms,
-                   "chunks": n_launch, "seed": args.seed},
+                   "chunks": n_launch, "seed": args.seed,
+                   "pt_pitch_words": hy_pitch, "pt_row_words": cfg.L * cfg.N},
         "achieved_alg_GBps": round(hy_gbs, 1),
         "roofline": {"bound": "hbm", "achieved": round(hy_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(hy_gbs / HBM_PEAK_GBS, 4),

@@ -86,6 +86,9 @@ void fiona_ctx_destroy(fiona_ctx *ctx);
 #define FIONA_PLAN_NO_PARTIAL_SHARING 8u   /* share only whole signed sums, no common sub-sums */
 #define FIONA_PLAN_PER_CONTRIBUTION 16u    /* no grouping: a scalar product per nonzero signed term
                                               (the first compilation of Sec. 6.2; implies NO_SHARING) */
+#define FIONA_PLAN_NO_OUTPUT_BURSTS 32u    /* store each output as soon as it is finished instead of
+                                              buffering a round of outputs in LDS and writing them together
+                                              (the default when outputs are at least 2.5% of the bytes) */
 
 /*
  * One routed layer, in the raw per-(output, term) form the offline compiler
@@ -104,6 +107,12 @@ void fiona_ctx_destroy(fiona_ctx *ctx);
  *                          values the caller later passes as ternary_groups
  *   grp_scale[n_group]     index into the scales array of each group (< n_scale)
  * n_group and n_member are grp_off[n_out] and grp_mem_off[n_group].
+ * Plaintext table layout:
+ *   pt_pitch               words from one plaintext to the next in pt_diags:
+ *                          0 means L*N (packed rows), otherwise at least L*N
+ *                          (FIONA_ERR_ARG if less).  Words between rows are
+ *                          never read.  fiona_pt_pitch_hint gives a padded
+ *                          pitch that spreads the rows over the HBM banks.
  */
 typedef struct fiona_layer_desc {
   uint32_t n_in, n_out, n_pt, n_scale;
@@ -116,7 +125,18 @@ typedef struct fiona_layer_desc {
   const int8_t *mem_sign;
   const uint32_t *grp_scale;
   uint32_t flags;
+  uint64_t pt_pitch;
 } fiona_layer_desc;
+
+/*
+ * fiona_pt_pitch_hint: a plaintext pitch for fiona_layer_desc.pt_pitch (in
+ * words) that keeps the rows streamed together by one launch off the same
+ * HBM banks: L*N rounded up to a multiple of 64 words, plus 128 words.  With
+ * packed rows (pitch L*N, a multiple of 2 MiB at N = 2^16) every plaintext's
+ * slice of a tile lands at the same bank offset; the padding spreads them.
+ * Returns 0 for a null ctx.
+ */
+uint64_t fiona_pt_pitch_hint(const fiona_ctx *ctx);
 
 /*
  * fiona_plan_create: compile one layer for the GPU.
@@ -141,8 +161,8 @@ typedef struct fiona_layer_desc {
  *   - uploads the compiled metadata to the current HIP device (synchronous)
  *     unless FIONA_PLAN_HOST_ONLY.
  * The plan keeps a reference to ctx (which must outlive it).  Errors:
- * FIONA_ERR_ARG, FIONA_ERR_PLAN, FIONA_ERR_UNSUPPORTED (more than FIONA_MAX_INPUTS
- * inputs, or a plaintext table beyond 2^48 bytes), FIONA_ERR_NOMEM, FIONA_ERR_HIP.
+ * FIONA_ERR_ARG (also a pt_pitch below L*N), FIONA_ERR_PLAN, FIONA_ERR_UNSUPPORTED
+ * (more than FIONA_MAX_INPUTS inputs, or a plaintext table beyond 2^48 bytes), FIONA_ERR_NOMEM, FIONA_ERR_HIP.
  * The plan owns a small device
  * workspace (the members of its signed sums, reordered by sign on every call),
  * so one plan must not be used by two streams at the same time.
@@ -174,6 +194,8 @@ typedef struct fiona_plan_stats_t {
   uint32_t segment_slots;          /* LDS rows holding the segments' partial residues */
   uint32_t n_partial;              /* common partial sums, each formed once per tile in LDS */
   uint32_t partial_levels;         /* longest chain of common terms built from common terms */
+  uint32_t output_rounds;          /* rounds of outputs per tile, each ending in one burst of stores */
+  uint32_t output_buffer_rows;     /* LDS rows (outputs) buffered per round; 0 = stored directly */
 } fiona_plan_stats_t;
 
 int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);
@@ -182,7 +204,9 @@ int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);
  * fiona_hybrid_linear: evaluate the layer (the hot path).
  *   in_cts          device, [n_in][2][L][N] uint64, every value < 2^50
  *                   (CKKS residues are < q_l)
- *   pt_diags        device, [n_pt][L][N] uint64 NTT-domain plaintexts, < 2^50
+ *   pt_diags        device, n_pt plaintexts of [L][N] uint64 NTT-domain
+ *                   residues < 2^50, plaintext p starting at word p * pitch
+ *                   (pitch = the plan's pt_pitch, L*N by default)
  *   ternary_groups  device, [n_member] int8 signs in {-1, 0, +1}, in the
  *                   member order of the layer description; must equal the
  *                   mem_sign the plan was created with (members that were 0

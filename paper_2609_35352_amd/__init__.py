@@ -10,7 +10,8 @@ the library has not been built, importing works but every call raises.
 
 Tensors are device tensors of 8-byte elements (uint64 residues, stored in any
 8-byte dtype) for in/pt/scale/out and int8 for the signs, laid out as the
-header describes: in [n_in][2][L][N], pt [n_pt][L][N], out [n_out][2][L][N].
+header describes: in [n_in][2][L][N], pt n_pt rows of [L][N] at the plan's
+pitch (default L*N), out [n_out][2][L][N].
 """
 from __future__ import annotations
 
@@ -27,6 +28,7 @@ FIONA_PLAN_HOST_ONLY = 2
 FIONA_PLAN_NO_LDS_SUMS = 4
 FIONA_PLAN_NO_PARTIAL_SHARING = 8
 FIONA_PLAN_PER_CONTRIBUTION = 16
+FIONA_PLAN_NO_OUTPUT_BURSTS = 32
 
 STATUS = {0: "FIONA_OK", -1: "FIONA_ERR_ARG", -2: "FIONA_ERR_PLAN", -3: "FIONA_ERR_UNSUPPORTED",
           -4: "FIONA_ERR_ALIGN", -5: "FIONA_ERR_ALIAS", -6: "FIONA_ERR_HIP", -7: "FIONA_ERR_NOMEM",
@@ -45,7 +47,7 @@ class _LayerDesc(ctypes.Structure):
                 ("pm_off", ctypes.c_void_p), ("pm_input", ctypes.c_void_p), ("pm_pt", ctypes.c_void_p),
                 ("grp_off", ctypes.c_void_p), ("grp_mem_off", ctypes.c_void_p),
                 ("mem_input", ctypes.c_void_p), ("mem_sign", ctypes.c_void_p), ("grp_scale", ctypes.c_void_p),
-                ("flags", ctypes.c_uint32)]
+                ("flags", ctypes.c_uint32), ("pt_pitch", ctypes.c_uint64)]
 
 
 class _Stats(ctypes.Structure):
@@ -53,7 +55,8 @@ class _Stats(ctypes.Structure):
         "ct_terms", "n_pmult", "n_member", "n_member_nonzero", "n_use", "n_sum_distinct", "n_sum_resident",
         "pmult_per_contribution", "pmult_grouped", "addsub_unshared", "addsub_shared", "addsub_partial")] + \
         [(n, ctypes.c_uint32) for n in ("tile", "waves", "lds_bytes", "grid", "split_outputs", "segment_slots",
-                                        "n_partial", "partial_levels")]
+                                        "n_partial", "partial_levels", "output_rounds",
+                                        "output_buffer_rows")]
 
 
 _lib = None
@@ -81,6 +84,8 @@ def lib():
         L.fiona_plan_stats.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Stats)]
         L.fiona_hybrid_linear.restype = ctypes.c_int
         L.fiona_hybrid_linear.argtypes = [ctypes.c_void_p] * 7
+        L.fiona_pt_pitch_hint.restype = ctypes.c_uint64
+        L.fiona_pt_pitch_hint.argtypes = [ctypes.c_void_p]
         L.fiona_status_string.restype = ctypes.c_char_p
         L.fiona_status_string.argtypes = [ctypes.c_int]
         _lib = L
@@ -108,6 +113,10 @@ class Ctx:
     def handle(self):
         return self._h
 
+    def pt_pitch_hint(self) -> int:
+        """fiona_pt_pitch_hint: a padded plaintext pitch (words) for this context."""
+        return int(lib().fiona_pt_pitch_hint(self._h))
+
     def close(self):
         if getattr(self, "_h", None) and self._h.value:
             lib().fiona_ctx_destroy(self._h)
@@ -128,7 +137,7 @@ class Plan:
     """A compiled layer (fiona_plan_create)."""
 
     def __init__(self, ctx: Ctx, n_in, n_out, n_pt, n_scale, pm_off, pm_input, pm_pt, grp_off, grp_mem_off,
-                 mem_input, mem_sign, grp_scale, flags: int = 0):
+                 mem_input, mem_sign, grp_scale, flags: int = 0, pt_pitch: int = 0):
         self.ctx = ctx
         keep = [_u32(pm_off), _u32(pm_input), _u32(pm_pt), _u32(grp_off), _u32(grp_mem_off),
                 _u32(mem_input), np.ascontiguousarray(mem_sign, dtype=np.int8), _u32(grp_scale)]
@@ -136,18 +145,24 @@ class Plan:
         def ptr(a):
             return a.ctypes.data if a.size else None
 
-        d = _LayerDesc(int(n_in), int(n_out), int(n_pt), int(n_scale), *[ptr(a) for a in keep], int(flags))
+        d = _LayerDesc(int(n_in), int(n_out), int(n_pt), int(n_scale), *[ptr(a) for a in keep], int(flags),
+                       int(pt_pitch))
         h = ctypes.c_void_p()
         _check(lib().fiona_plan_create(ctx.handle, ctypes.byref(d), ctypes.byref(h)), "fiona_plan_create")
         self._h = h
         self.n_in, self.n_out, self.n_pt, self.n_scale = int(n_in), int(n_out), int(n_pt), int(n_scale)
         self.n_member = int(keep[4][-1]) if keep[4].size else 0
+        self.pt_pitch = int(pt_pitch) if pt_pitch else ctx.L * ctx.N
 
     @classmethod
-    def from_layer(cls, ctx: Ctx, layer, flags: int = 0) -> "Plan":
+    def from_layer(cls, ctx: Ctx, layer, flags: int = 0, pt_pitch: int = 0) -> "Plan":
         return cls(ctx, layer.n_in, layer.n_out, layer.n_pt, len(layer.scales), layer.pm_off, layer.pm_input,
                    layer.pm_pt, layer.grp_off, layer.grp_mem_off, layer.mem_input, layer.mem_sign,
-                   layer.grp_scale, flags)
+                   layer.grp_scale, flags, pt_pitch)
+
+    def pt_words(self) -> int:
+        """Words the plaintext table spans under this plan's pitch."""
+        return (self.n_pt - 1) * self.pt_pitch + self.ctx.L * self.ctx.N if self.n_pt else 0
 
     @property
     def handle(self):
@@ -187,7 +202,7 @@ def hybrid_linear(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t, stream=None) -
     import torch
 
     N, L = plan.ctx.N, plan.ctx.L
-    sizes = [(in_t, "in_cts", plan.n_in * 2 * L * N), (pt_t, "pt_diags", plan.n_pt * L * N),
+    sizes = [(in_t, "in_cts", plan.n_in * 2 * L * N), (pt_t, "pt_diags", plan.pt_words()),
              (out_t, "out_cts", plan.n_out * 2 * L * N), (sign_t, "ternary_groups", plan.n_member),
              (scale_t, "scales", plan.n_scale)]
     for t, name, n in sizes:

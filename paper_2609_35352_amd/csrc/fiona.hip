@@ -25,6 +25,8 @@ constexpr uint32_t kSlotBytes = fiona::kTile * 16u;   // one input or sum tile i
 constexpr uint32_t kMaxInputs = kLdsBytes / kSlotBytes;   // LDS rows of one workgroup
 static_assert(FIONA_MAX_INPUTS + 1 == kMaxInputs, "inputs plus the zero row fill the LDS");
 constexpr uint32_t kMaxSegments = 64;           // segments of one split output
+constexpr uint32_t kMinBurstRows = 8;           // free LDS rows needed for output bursts
+constexpr double kMinBurstShare = 0.025;        // output share of a launch's HBM bytes for bursts
 // Relative costs used to balance work items over wavefronts (units: one raw term).
 constexpr double kCostUseResident = 0.6;
 constexpr double kCostUseInline = 0.5;
@@ -61,6 +63,7 @@ bool ranges_overlap(const void *a, size_t na, const void *b, size_t nb) {
 struct fiona_plan {
   const fiona_ctx *ctx = nullptr;
   uint32_t n_in = 0, n_out = 0, n_pt = 0, n_scale = 0, n_member_desc = 0;
+  uint64_t pt_pitch = 0;   // words from one plaintext to the next
   uint32_t n_mat = 0;
   uint32_t n_part = 0, n_levels = 0;   // common partial sums and their levels
   std::vector<uint32_t> part_levels;
@@ -68,8 +71,11 @@ struct fiona_plan {
   fiona_plan_stats_t st{};
   std::vector<uint4> items;
   std::vector<uint32_t> dest;
-  std::vector<uint2> waves;
+  std::vector<uint2> waves;    // [n_rounds][nw]
   std::vector<uint4> splits;
+  std::vector<uint4> rounds;   // per round: first flush entry, buffered outputs, first split, split outputs
+  std::vector<uint32_t> flush; // output index of each buffered output, round by round
+  uint32_t n_rounds = 1, obuf_rows = 0;
   uint32_t nw = 8, n_seg_slots = 0;
   std::vector<uint2> pm;
   std::vector<uint4> uses;
@@ -80,8 +86,8 @@ struct fiona_plan {
   int device = -1;
   // device pointers into dev
   const LimbConst *d_limbs = nullptr;
-  const uint4 *d_items = nullptr, *d_splits = nullptr, *d_uses = nullptr;
-  const uint32_t *d_dest = nullptr;
+  const uint4 *d_items = nullptr, *d_splits = nullptr, *d_uses = nullptr, *d_rounds = nullptr;
+  const uint32_t *d_dest = nullptr, *d_flush = nullptr;
   const uint2 *d_waves = nullptr, *d_pm = nullptr, *d_members = nullptr, *d_sums = nullptr;
   const uint32_t *d_mats = nullptr;
   uint32_t *d_words = nullptr;
@@ -131,6 +137,12 @@ int fiona_ctx_create(uint32_t N, uint32_t L, const uint64_t *moduli, fiona_ctx *
 }
 
 void fiona_ctx_destroy(fiona_ctx *ctx) { delete ctx; }
+
+uint64_t fiona_pt_pitch_hint(const fiona_ctx *ctx) {
+  if (!ctx) return 0;
+  const uint64_t ln = (uint64_t)ctx->L * ctx->N;
+  return (ln + 63) / 64 * 64 + 128;
+}
 
 }  // extern "C"
 
@@ -364,6 +376,16 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   // One workgroup per CU when the LDS image exceeds half the CU: then 16 wavefronts.
   const uint32_t est_slots = d->n_in + n_part + std::min<uint32_t>((uint32_t)cand.size(), rows_free);
   P->nw = est_slots * 2 > kMaxInputs ? 16 : 8;
+  // Output bursts: one workgroup per CU (16 wavefronts) that keeps finished
+  // outputs in the LDS rows its image leaves free and writes them together at
+  // the end of a round.  Output stores spread among the plaintext reads cost
+  // far more HBM time than the same bytes written in bursts.
+  // They pay when outputs are a fair share of the launch's bytes; else one
+  // workgroup per CU and the barriers that end the rounds cost more.
+  const double out_share = 2.0 * d->n_out / (2.0 * d->n_in + (double)n_pm + 2.0 * d->n_out);
+  bool bursts = !(d->flags & FIONA_PLAN_NO_OUTPUT_BURSTS) && d->n_out > 0 && out_share >= kMinBurstShare &&
+                est_slots + 1 + kMinBurstRows <= kMaxInputs;
+  if (bursts) P->nw = 16;
 
   // Work items: whole outputs, or segments of outputs that are long compared
   // with the share of one wavefront.
@@ -396,6 +418,33 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   if (cand.size() > rows_free - seg_slots) {   // segments take precedence over the least used residents
     for (size_t c = rows_free - seg_slots; c < cand.size(); ++c) resident[cand[c]] = 0;
     cand.resize(rows_free - seg_slots);
+  }
+  // Rounds of outputs: consecutive outputs, as many whole (unsplit) outputs per
+  // round as the free LDS rows hold.
+  std::vector<uint32_t> round_of(d->n_out, 0);
+  {
+    const uint32_t image = d->n_in + n_part + (uint32_t)cand.size() + seg_slots + 1;
+    const uint32_t avail = kMaxInputs > image ? kMaxInputs - image : 0;
+    uint32_t n_whole = 0;
+    for (uint32_t j = 0; j < d->n_out; ++j) n_whole += nseg[j] == 1;
+    if (avail < kMinBurstRows || n_whole == 0) bursts = false;
+    P->n_rounds = 1;
+    if (bursts) {
+      uint32_t n_rounds = (n_whole + avail - 1) / avail;
+      for (;; ++n_rounds) {   // outputs in order, evenly over the rounds
+        std::vector<uint32_t> cnt(n_rounds, 0);
+        uint32_t most = 0;
+        for (uint32_t j = 0; j < d->n_out; ++j) {
+          round_of[j] = (uint32_t)((uint64_t)j * n_rounds / d->n_out);
+          if (nseg[j] == 1) most = std::max(most, ++cnt[round_of[j]]);
+        }
+        if (most <= avail) {
+          P->obuf_rows = most;
+          break;
+        }
+      }
+      P->n_rounds = n_rounds;
+    }
   }
 
   // Device records.  Words: one block per common partial sum, then one per
@@ -459,7 +508,7 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   // are sorted by plaintext offset: a chunk then covers a short stretch of the
   // plaintext table, and its terms' offsets from the chunk base fit 31 bits.
   const uint32_t zero_row = d->n_in + n_part + (uint32_t)P->mats.size() + seg_slots;
-  const uint64_t ln8 = (uint64_t)P->ctx->L * P->ctx->N * 8;
+  const uint64_t ln8 = P->pt_pitch * 8;
   auto emit_chunks = [&](const std::vector<std::pair<uint64_t, uint32_t>> &terms, size_t t0, size_t t1) {
     const uint32_t first = (uint32_t)(P->pm.size() / fiona::kChunkSlots);
     size_t t = t0;
@@ -479,10 +528,28 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
     return make_uint2(first, (uint32_t)(P->pm.size() / fiona::kChunkSlots) - first);
   };
 
-  // items, each with its cost; segments of a split output get consecutive LDS slots
-  struct Item { uint4 rec; uint32_t dest; double cost; };
+  // items, each with its cost; segments of a split output get consecutive LDS
+  // slots; buffered outputs get the next row of their round's output buffer
+  struct Item { uint4 rec; uint32_t dest; double cost; uint32_t round; };
   std::vector<Item> items;
   uint32_t slot = 0;
+  P->rounds.assign(P->n_rounds, make_uint4(0, 0, 0, 0));
+  for (uint32_t j = 0, r = 0; j < d->n_out; ++j) {   // first entries of each round
+    for (; r < round_of[j]; ++r) {
+      P->rounds[r + 1].x = P->rounds[r].x + P->rounds[r].y;
+      P->rounds[r + 1].z = P->rounds[r].z + P->rounds[r].w;
+    }
+    if (nseg[j] > 1) P->rounds[r].w++;
+    else if (bursts) P->rounds[r].y++;
+  }
+  for (uint32_t r = 1; r < P->n_rounds; ++r) {   // rounds after the last output's
+    if (P->rounds[r].x < P->rounds[r - 1].x + P->rounds[r - 1].y) {
+      P->rounds[r].x = P->rounds[r - 1].x + P->rounds[r - 1].y;
+      P->rounds[r].z = P->rounds[r - 1].z + P->rounds[r - 1].w;
+    }
+  }
+  P->flush.assign(P->rounds.empty() ? 0 : P->rounds.back().x + P->rounds.back().y, 0);
+  std::vector<uint32_t> buf_row(P->n_rounds, 0);
   std::vector<std::pair<uint64_t, uint32_t>> terms;   // (plaintext byte offset, input)
   for (uint32_t j = 0; j < d->n_out; ++j) {
     const uint32_t pb = d->pm_off[j], pc = d->pm_off[j + 1] - pb;
@@ -501,28 +568,39 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
       const uint2 ch = emit_chunks(terms, r0, r1);
       double c = kCostFinish + (double)(r1 - r0) + kCostChunk * ch.y;
       for (uint32_t u = u0; u < u1; ++u) c += use_cost(out_uses[j][u]);
-      items.push_back(Item{make_uint4(ch.x, ch.y, ub + u0, u1 - u0),
-                           S > 1 ? (fiona::kSegmentFlag | (slot + g)) : j, c});
+      uint32_t dst = j;
+      if (S > 1) {
+        dst = fiona::kSegmentFlag | (slot + g);
+      } else if (bursts) {
+        const uint32_t r = round_of[j], row = buf_row[r]++;
+        P->flush[P->rounds[r].x + row] = j;
+        dst = fiona::kBufferFlag | row;
+      }
+      items.push_back(Item{make_uint4(ch.x, ch.y, ub + u0, u1 - u0), dst, c, round_of[j]});
     }
     if (S > 1) slot += S;
   }
-  // longest item first onto the least loaded wavefront
-  std::vector<uint32_t> order(items.size());
-  for (uint32_t t = 0; t < order.size(); ++t) order[t] = t;
-  std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return items[a].cost > items[b].cost; });
-  std::vector<double> load(P->nw, 0.0);
-  std::vector<std::vector<uint32_t>> per_wave(P->nw);
-  for (uint32_t t : order) {
-    const uint32_t w = (uint32_t)(std::min_element(load.begin(), load.end()) - load.begin());
-    load[w] += items[t].cost;
-    per_wave[w].push_back(t);
-  }
-  for (uint32_t w = 0; w < P->nw; ++w) {
-    std::sort(per_wave[w].begin(), per_wave[w].end());
-    P->waves.push_back(make_uint2((uint32_t)P->items.size(), (uint32_t)per_wave[w].size()));
-    for (uint32_t t : per_wave[w]) {
-      P->items.push_back(items[t].rec);
-      P->dest.push_back(items[t].dest);
+  // per round: longest item first onto the least loaded wavefront
+  for (uint32_t r = 0; r < P->n_rounds; ++r) {
+    std::vector<uint32_t> order;
+    for (uint32_t t = 0; t < items.size(); ++t)
+      if (items[t].round == r) order.push_back(t);
+    std::stable_sort(order.begin(), order.end(),
+                     [&](uint32_t a, uint32_t b) { return items[a].cost > items[b].cost; });
+    std::vector<double> load(P->nw, 0.0);
+    std::vector<std::vector<uint32_t>> per_wave(P->nw);
+    for (uint32_t t : order) {
+      const uint32_t w = (uint32_t)(std::min_element(load.begin(), load.end()) - load.begin());
+      load[w] += items[t].cost;
+      per_wave[w].push_back(t);
+    }
+    for (uint32_t w = 0; w < P->nw; ++w) {
+      std::sort(per_wave[w].begin(), per_wave[w].end());
+      P->waves.push_back(make_uint2((uint32_t)P->items.size(), (uint32_t)per_wave[w].size()));
+      for (uint32_t t : per_wave[w]) {
+        P->items.push_back(items[t].rec);
+        P->dest.push_back(items[t].dest);
+      }
     }
   }
 
@@ -550,7 +628,9 @@ int upload_plan(fiona_plan *P) {
   const size_t o_dest = align_up(o_items + sizeof(uint4) * P->items.size(), a);
   const size_t o_waves = align_up(o_dest + sizeof(uint32_t) * P->dest.size(), a);
   const size_t o_splits = align_up(o_waves + sizeof(uint2) * P->waves.size(), a);
-  const size_t o_pm = align_up(o_splits + sizeof(uint4) * P->splits.size(), a);
+  const size_t o_rounds = align_up(o_splits + sizeof(uint4) * P->splits.size(), a);
+  const size_t o_flush = align_up(o_rounds + sizeof(uint4) * P->rounds.size(), a);
+  const size_t o_pm = align_up(o_flush + sizeof(uint32_t) * P->flush.size(), a);
   const size_t o_uses = align_up(o_pm + sizeof(uint2) * P->pm.size(), a);
   const size_t o_mats = align_up(o_uses + sizeof(uint4) * P->uses.size(), a);
   const size_t o_mem = align_up(o_mats + sizeof(uint32_t) * P->mats.size(), a);
@@ -565,6 +645,8 @@ int upload_plan(fiona_plan *P) {
   put(o_dest, P->dest.data(), sizeof(uint32_t) * P->dest.size());
   put(o_waves, P->waves.data(), sizeof(uint2) * P->waves.size());
   put(o_splits, P->splits.data(), sizeof(uint4) * P->splits.size());
+  put(o_rounds, P->rounds.data(), sizeof(uint4) * P->rounds.size());
+  put(o_flush, P->flush.data(), sizeof(uint32_t) * P->flush.size());
   put(o_pm, P->pm.data(), sizeof(uint2) * P->pm.size());
   put(o_uses, P->uses.data(), sizeof(uint4) * P->uses.size());
   put(o_mats, P->mats.data(), sizeof(uint32_t) * P->mats.size());
@@ -591,6 +673,8 @@ int upload_plan(fiona_plan *P) {
   P->d_dest = (const uint32_t *)(base + o_dest);
   P->d_waves = (const uint2 *)(base + o_waves);
   P->d_splits = (const uint4 *)(base + o_splits);
+  P->d_rounds = (const uint4 *)(base + o_rounds);
+  P->d_flush = (const uint32_t *)(base + o_flush);
   P->d_pm = (const uint2 *)(base + o_pm);
   P->d_uses = (const uint4 *)(base + o_uses);
   P->d_mats = (const uint32_t *)(base + o_mats);
@@ -611,14 +695,18 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   int rc = validate_desc(desc);
   if (rc != FIONA_OK) return rc;
   if (desc->n_in > FIONA_MAX_INPUTS) return FIONA_ERR_UNSUPPORTED;
+  const uint64_t ln = (uint64_t)ctx->L * ctx->N;
+  const uint64_t pitch = desc->pt_pitch ? desc->pt_pitch : ln;
+  if (pitch < ln || pitch > (1ull << 45)) return FIONA_ERR_ARG;
   // raw-term records hold 48-bit byte offsets into the plaintext table
-  if ((uint64_t)desc->n_pt * ctx->L * ctx->N * 8 > (1ull << 48)) return FIONA_ERR_UNSUPPORTED;
+  if (((uint64_t)desc->n_pt * pitch) * 8 > (1ull << 48)) return FIONA_ERR_UNSUPPORTED;
   fiona_plan *P = new (std::nothrow) fiona_plan;
   if (!P) return FIONA_ERR_NOMEM;
   P->ctx = ctx;
   P->n_in = desc->n_in;
   P->n_out = desc->n_out;
   P->n_pt = desc->n_pt;
+  P->pt_pitch = pitch;
   P->n_scale = desc->n_scale;
   P->flags = desc->flags;
   try {
@@ -632,11 +720,13 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   }
   P->tiles = (ctx->N + fiona::kTile - 1) / fiona::kTile;
   P->grid = P->tiles * ctx->L;
-  P->lds_bytes = (P->n_in + P->n_part + P->n_mat + P->n_seg_slots + 1) * kSlotBytes;
+  P->lds_bytes = (P->n_in + P->n_part + P->n_mat + P->n_seg_slots + 1 + P->obuf_rows) * kSlotBytes;
   P->st.tile = fiona::kTile;
   P->st.waves = P->nw;
   P->st.split_outputs = (uint32_t)P->splits.size();
   P->st.segment_slots = P->n_seg_slots;
+  P->st.output_rounds = P->n_rounds;
+  P->st.output_buffer_rows = P->obuf_rows;
   P->st.lds_bytes = P->lds_bytes;
   P->st.grid = P->grid;
   KShape &k = P->shape;
@@ -644,8 +734,9 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   k.L = ctx->L;
   k.n_in = P->n_in;
   k.n_mat = P->n_mat;
-  k.n_split = (uint32_t)P->splits.size();
   k.zero_row = P->n_in + P->n_part + P->n_mat + P->n_seg_slots;
+  k.n_rounds = P->n_rounds;
+  k.obuf_row = k.zero_row + 1;
   k.n_part = P->n_part;
   k.n_levels = P->n_levels;
   for (uint32_t l = 0; l < fiona::kMaxLevels; ++l) k.level_end[l] = P->part_levels[l];
@@ -681,7 +772,7 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   const fiona_ctx *C = plan->ctx;
   const size_t LN = (size_t)C->L * C->N;
   const size_t in_bytes = (size_t)plan->n_in * 2 * LN * 8;
-  const size_t pt_bytes = (size_t)plan->n_pt * LN * 8;
+  const size_t pt_bytes = plan->n_pt ? ((size_t)(plan->n_pt - 1) * plan->pt_pitch + LN) * 8 : 0;
   const size_t out_bytes = (size_t)plan->n_out * 2 * LN * 8;
   const size_t sign_bytes = plan->n_member_desc;
   const size_t scale_bytes = (size_t)plan->n_scale * 8;
@@ -718,9 +809,20 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
     if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   }
   auto kernel = plan->nw == 16 ? fiona::hybrid_linear_kernel<16> : fiona::hybrid_linear_kernel<8>;
+  fiona::KPlan kp;
+  kp.limbs = plan->d_limbs;
+  kp.items = plan->d_items;
+  kp.dest = plan->d_dest;
+  kp.waves = plan->d_waves;
+  kp.rounds = plan->d_rounds;
+  kp.flush = plan->d_flush;
+  kp.splits = plan->d_splits;
+  kp.pm = plan->d_pm;
+  kp.uses = plan->d_uses;
+  kp.mats = plan->d_mats;
+  kp.words = plan->d_words;
   hipLaunchKernelGGL(kernel, dim3(plan->grid), dim3(plan->nw * 64), plan->lds_bytes, stream, in_cts, pt_diags,
-                     out_cts, plan->d_limbs, plan->d_items, plan->d_dest, plan->d_waves, plan->d_splits,
-                     plan->d_pm, plan->d_uses, plan->d_mats, plan->d_words, plan->shape);
+                     out_cts, kp, plan->shape);
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   return FIONA_OK;
 }

@@ -41,10 +41,12 @@ constexpr uint32_t kChunkSlots = 64;      // records per chunk block; the last o
 constexpr uint32_t kSumBatch = 4;         // member reads issued before their additions
 constexpr uint32_t kSumBatches = kMaxMembers / kSumBatch;
 constexpr uint32_t kSumWords = 64;        // words per distinct sum: header + padded member rows
-constexpr uint32_t kSegmentFlag = 0x80000000u;
+constexpr uint32_t kSegmentFlag = 0x80000000u;   // item destination: a segment slot in LDS
+constexpr uint32_t kBufferFlag = 0x40000000u;    // item destination: a row of the output buffer in LDS
 constexpr uint32_t kNormaliseSigns = 0x80000000u;   // block flag: signs relative to the first member's
 constexpr uint32_t kMaxLevels = 4;        // levels of common partial sums
 constexpr int kLoadNT = 2;                // cache policy of the plaintext stream: nontemporal
+constexpr int kStoreSc1 = 16;             // cache policy of the output stores: sc1 (device scope)
 static_assert(kChunkTerms % kRawBatch == 0 && kChunkTerms < kChunkSlots, "chunk layout");
 // header, rows to add from word 1 up, rows to subtract from word 62 down, each list padded to a batch
 static_assert(1 + kMaxMembers + 2 * (kSumBatch - 1) <= kSumWords - 1, "sum block layout");
@@ -64,9 +66,11 @@ struct PackParams {
 
 // Scalars of the main kernel.  LDS rows: inputs, common partial sums (level by
 // level; level l ends at level_end[l]), resident signed sums, segment slots,
-// the zero row.
+// the zero row, then the output buffer (from row obuf_row).  The outputs are
+// produced in n_rounds rounds; each round ends with a barrier after which the
+// round's buffered outputs and split outputs are written out together.
 struct KShape {
-  uint32_t N, L, n_in, n_part, n_levels, n_mat, n_split, zero_row, tiles;
+  uint32_t N, L, n_in, n_part, n_levels, n_mat, zero_row, tiles, n_rounds, obuf_row;
   uint32_t level_end[kMaxLevels];
 };
 
@@ -219,6 +223,18 @@ __device__ __forceinline__ void raw_chunk(uint32_t nb, __amdgpu_buffer_rsrc_t rs
   }
 }
 
+// Stores one output position of both polynomials: row = the output's limb
+// row at this tile (polynomial 0), poly_bytes = the distance to polynomial 1.
+// Device-scope stores write through the XCD's L2, so the outputs leave the
+// chip together instead of as scattered L2 evictions among the plaintext reads.
+__device__ __forceinline__ void store_out(uint64_t *row, uint32_t lane_bytes, uint32_t poly_bytes, uint64_t y0,
+                                          uint64_t y1) {
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)row, (short)0, (int)0xFFFFFFFF, 0x00020000);
+  __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y0, (uint32_t)(y0 >> 32)}, rs, lane_bytes, 0, kStoreSc1);
+  __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y1, (uint32_t)(y1 >> 32)}, rs, lane_bytes + poly_bytes, 0,
+                                        kStoreSc1);
+}
+
 __device__ __forceinline__ void fold(Acc &a0, Acc &a1, uint64_t &r0, uint64_t &r1, const LimbConst &lc) {
   r0 = finish(a0, r0, lc);
   r1 = finish(a1, r1, lc);
@@ -233,13 +249,33 @@ __device__ __forceinline__ uint4 load_use_chunk(const uint4 *uses, uint32_t begi
   return lane < count ? uses[begin + lane] : make_uint4(0, kInlineSum, 0, 0);
 }
 
+// Plan records of the main kernel (device pointers into the plan's image).
+struct KPlan {
+  const LimbConst *limbs;   // [L]
+  const uint4 *items;       // per work item: first chunk, chunks, first use, uses
+  const uint32_t *dest;     // per work item: output, kSegmentFlag | slot or kBufferFlag | row
+  const uint2 *waves;       // per (round, wavefront): first item, item count
+  const uint4 *rounds;      // per round: first flush entry, buffered outputs, first split, split outputs
+  const uint32_t *flush;    // per buffered output: its output index (buffer row = entry - first)
+  const uint4 *splits;      // per split output: output, first segment slot, segments
+  const uint2 *pm;          // raw-term chunk blocks
+  const uint4 *uses;        // signed-sum uses
+  const uint32_t *mats;     // per resident sum: its word block
+  const uint32_t *words;    // word blocks of the common partial sums and distinct signed sums
+};
+
 template <int NW>
-__global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
-    const uint64_t *__restrict__ in, const uint64_t *__restrict__ pt, uint64_t *__restrict__ out, const LimbConst *__restrict__ limbs, const uint4 *__restrict__ items,
-    const uint32_t *__restrict__ dest, const uint2 *__restrict__ waves, const uint4 *__restrict__ splits,
-    const uint2 *__restrict__ pm, const uint4 *__restrict__ uses, const uint32_t *__restrict__ mats,
-    const uint32_t *__restrict__ words, const KShape S) {
-  extern __shared__ uint4 lds[];   // [n_in + n_part + n_mat + segment slots + zero row][kTile]
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4, 4))) hybrid_linear_kernel(
+    const uint64_t *__restrict__ in, const uint64_t *__restrict__ pt, uint64_t *__restrict__ out, const KPlan K,
+    const KShape S) {
+  extern __shared__ uint4 lds[];   // [n_in + n_part + n_mat + segment slots + zero row + output buffer][kTile]
+  const LimbConst *__restrict__ limbs = K.limbs;
+  const uint4 *__restrict__ items = K.items;
+  const uint32_t *__restrict__ dest = K.dest;
+  const uint2 *__restrict__ pm = K.pm;
+  const uint4 *__restrict__ uses = K.uses;
+  const uint32_t *__restrict__ mats = K.mats;
+  const uint32_t *__restrict__ words = K.words;
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t lane16 = lane * 16u;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -285,12 +321,15 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
     __syncthreads();
   }
 
-  // 4. this wavefront's work items; the first records of each item are loaded
-  // while the previous item runs
+  // 4. this wavefront's work items of each round; the first records of each
+  // item are loaded while the previous item runs
   uint4 *segs = sums + (size_t)S.n_mat * kTile;
+  uint4 *obuf = lds + (size_t)S.obuf_row * kTile;
   const char *pt_tile = (const char *)(pt + (size_t)limb * S.N + k0);
   const uint32_t voff = lane_off * 8u;
-  const uint2 wr = waves[wave];
+  const uint32_t out_row = limb * S.N + k0;   // offset of this tile in one output polynomial
+  for (uint32_t rd = 0; rd < S.n_rounds; ++rd) {
+  const uint2 wr = K.waves[rd * NW + wave];
   uint4 item_next = wr.y ? items[wr.x] : make_uint4(0, 0, 0, 0);
   uint2 raw_next = item_next.y ? load_chunk(pm, item_next.x, lane) : make_uint2(0, 0);
   uint4 use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
@@ -368,18 +407,21 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
     if (d & kSegmentFlag) {
       segs[(d & ~kSegmentFlag) * kTile + lane] =
           make_uint4((uint32_t)y0, (uint32_t)(y0 >> 32), (uint32_t)y1, (uint32_t)(y1 >> 32));
+    } else if (d & kBufferFlag) {
+      obuf[(d & ~kBufferFlag) * kTile + lane] =
+          make_uint4((uint32_t)y0, (uint32_t)(y0 >> 32), (uint32_t)y1, (uint32_t)(y1 >> 32));
     } else if (k < S.N) {
-      uint64_t *dst = out + ((size_t)d * 2 * S.L + limb) * S.N + k;
-      __builtin_nontemporal_store(y0, dst);
-      __builtin_nontemporal_store(y1, dst + LN);
+      store_out(out + (size_t)d * 2 * LN + out_row, lane * 8u, (uint32_t)(LN * 8), y0, y1);
     }
   }
 
-  // 5. outputs that were split across wavefronts: add their segments' residues
-  if (S.n_split) {
+  // 5. end of the round: outputs that were split across wavefronts add their
+  // segments' residues, and the buffered outputs leave LDS in one burst
+  const uint4 rr = K.rounds[rd];   // first flush entry, buffered outputs, first split, split outputs
+  if (rr.y | rr.w) {               // uniform over the workgroup
     __syncthreads();
-    for (uint32_t s = wave; s < S.n_split; s += NW) {
-      const uint4 sp = splits[s];
+    for (uint32_t s = wave; s < rr.w; s += NW) {
+      const uint4 sp = K.splits[rr.z + s];
       uint64_t y0 = 0, y1 = 0;   // at most 64 residues < 2^50: below 2^56
       for (uint32_t g = 0; g < sp.z; ++g) {
         const uint4 v = segs[(sp.y + g) * kTile + lane];
@@ -388,13 +430,17 @@ __global__ void __launch_bounds__(NW * 64) hybrid_linear_kernel(
       }
       y0 = reduce_i64((int64_t)y0, lc.q, lc.qinv);
       y1 = reduce_i64((int64_t)y1, lc.q, lc.qinv);
-      if (k < S.N) {
-        uint64_t *dst = out + ((size_t)sp.x * 2 * S.L + limb) * S.N + k;
-        __builtin_nontemporal_store(y0, dst);
-        __builtin_nontemporal_store(y1, dst + LN);
-      }
+      if (k < S.N) store_out(out + (size_t)sp.x * 2 * LN + out_row, lane * 8u, (uint32_t)(LN * 8), y0, y1);
     }
+    for (uint32_t e = wave; e < rr.y; e += NW) {
+      const uint4 v = obuf[e * kTile + lane];
+      const uint32_t j = K.flush[rr.x + e];
+      if (k < S.N)
+        store_out(out + (size_t)j * 2 * LN + out_row, lane * 8u, (uint32_t)(LN * 8), pair64(v.x, v.y), pair64(v.z, v.w));
+    }
+    if (rd + 1 < S.n_rounds) __syncthreads();   // the next round refills the buffer
   }
+  }   // rounds
 }
 
 }  // namespace fiona

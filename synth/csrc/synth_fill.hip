@@ -43,13 +43,13 @@ __global__ void __launch_bounds__(256) fill_rows_kernel(uint64_t *dst, uint32_t 
 // takes stream positions of its global id; a constant plaintext (pt_const >= 0,
 // sign code in bits 32..33, scale in bits 0..31) holds h*c mod q everywhere.
 __global__ void __launch_bounds__(256) fill_pts_kernel(uint64_t *dst, uint32_t n_pt, uint32_t L, uint32_t N,
-                                                       const uint64_t *pt_global, const int64_t *pt_const,
-                                                       uint64_t key, Moduli m) {
+                                                       uint64_t pitch, const uint64_t *pt_global,
+                                                       const int64_t *pt_const, uint64_t key, Moduli m) {
   const uint32_t r = blockIdx.x;
   const uint32_t p = r / L, l = r - p * L;
   if (p >= n_pt) return;
   const uint64_t q = m.q[l];
-  uint64_t *row = dst + (uint64_t)r * N;
+  uint64_t *row = dst + (uint64_t)p * pitch + (uint64_t)l * N;
   const int64_t c = pt_const ? pt_const[p] : -1;
   if (c >= 0) {
     const uint64_t code = (uint64_t)c >> 32, s = (uint64_t)c & 0xFFFFFFFFull;
@@ -87,18 +87,20 @@ int synth_fill_uniform(uint64_t *dst, uint32_t n_rows, uint32_t L, uint32_t N, u
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }
 
-// dst: device [n_pt][L][N]; pt_global: device [n_pt]; pt_const: device
-// [n_pt] or null.
-int synth_fill_pts(uint64_t *dst, uint32_t n_pt, uint32_t L, uint32_t N, const uint64_t *pt_global,
+// dst: device, n_pt plaintexts of [L][N], plaintext p at word p * pitch
+// (pitch >= L * N; the words between rows are left as they are);
+// pt_global: device [n_pt]; pt_const: device [n_pt] or null.
+int synth_fill_pts(uint64_t *dst, uint32_t n_pt, uint32_t L, uint32_t N, uint64_t pitch, const uint64_t *pt_global,
                    const int64_t *pt_const, uint64_t seed, uint64_t tag, const uint64_t *moduli_host,
                    hipStream_t stream) {
   Moduli m;
   if (!dst || !pt_global || N == 0 || make_moduli(moduli_host, L, &m) != 0) return -1;
+  if (pitch < (uint64_t)L * N) return -1;
   if (n_pt == 0) return 0;
   const uint64_t rows = (uint64_t)n_pt * L;
   if (rows >= (1ull << 31)) return -1;
-  hipLaunchKernelGGL(fill_pts_kernel, dim3((uint32_t)rows), dim3(256), 0, stream, dst, n_pt, L, N, pt_global,
-                     pt_const, stream_key(seed, tag), m);
+  hipLaunchKernelGGL(fill_pts_kernel, dim3((uint32_t)rows), dim3(256), 0, stream, dst, n_pt, L, N, pitch,
+                     pt_global, pt_const, stream_key(seed, tag), m);
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }
 

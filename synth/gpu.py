@@ -37,8 +37,8 @@ def lib():
                                          ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p]
         L.synth_fill_pts.restype = ctypes.c_int
         L.synth_fill_pts.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
-                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
-                                     ctypes.c_void_p, ctypes.c_void_p]
+                                     ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                                     ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -75,10 +75,13 @@ def fill_cts(layer: Layer, t, n_ct: int) -> None:
         raise RuntimeError("synth_fill_uniform failed (%d)" % rc)
 
 
-def fill_pts(layer: Layer, t) -> None:
-    """t: device tensor of >= n_pt*L*N 8-byte elements -> this layer's plaintext table."""
+def fill_pts(layer: Layer, t, pitch: int = 0) -> None:
+    """t: device tensor -> this layer's plaintext table, plaintext p at word p * pitch
+    (pitch 0 = L*N, packed rows); t needs (n_pt-1)*pitch + L*N 8-byte elements."""
     import torch
-    n = layer.n_pt * layer.L * layer.N
+    pitch = int(pitch) if pitch else layer.L * layer.N
+    assert pitch >= layer.L * layer.N
+    n = (layer.n_pt - 1) * pitch + layer.L * layer.N if layer.n_pt else 0
     assert t.is_cuda and t.is_contiguous() and t.element_size() == 8 and t.numel() >= n
     if layer.n_pt == 0:
         return
@@ -87,7 +90,7 @@ def fill_pts(layer: Layer, t) -> None:
     if layer.pt_const is not None:
         const = torch.from_numpy(np.ascontiguousarray(layer.pt_const.astype(np.int64))).to(t.device)
     m = _moduli(layer)
-    rc = lib().synth_fill_pts(t.data_ptr(), layer.n_pt, layer.L, layer.N, glob.data_ptr(),
+    rc = lib().synth_fill_pts(t.data_ptr(), layer.n_pt, layer.L, layer.N, pitch, glob.data_ptr(),
                               const.data_ptr() if const is not None else None, layer.seed, TAG_PT,
                               ctypes.cast(m, ctypes.c_void_p), _stream())
     if rc != 0:

@@ -100,6 +100,24 @@ def test_plan_validation_errors():
     assert e.value.status == -3
 
 
+def test_plaintext_pitch_checks():
+    """pt_pitch: 0 (packed) and anything >= L*N are accepted, a pitch below L*N is
+    FIONA_ERR_ARG; the hint is L*N rounded up to 64 words plus 128."""
+    lay = _small_layer()
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    ln = lay.L * lay.N
+    assert ctx.pt_pitch_hint() == (ln + 63) // 64 * 64 + 128
+    assert fiona.lib().fiona_pt_pitch_hint(None) == 0
+    for pitch in (0, ln, ln + 1, ctx.pt_pitch_hint()):
+        fiona.Plan(ctx, flags=HOST, pt_pitch=pitch, **_plan_args(lay)).close()
+    for pitch in (1, ln - 1):
+        with pytest.raises(fiona.FionaError) as e:
+            fiona.Plan(ctx, flags=HOST, pt_pitch=pitch, **_plan_args(lay))
+        assert e.value.status == -1
+    ctx2 = fiona.Ctx(1000, 3, synth.ntt_primes(1024, 3))
+    assert ctx2.pt_pitch_hint() == 3008 + 128
+
+
 def test_hybrid_linear_error_paths_without_device():
     lay = _small_layer()
     ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
@@ -174,8 +192,30 @@ def test_config_plans(name):
     if name == "vit768":
         assert st["n_sum_distinct"] <= 48 and st["n_sum_resident"] == st["n_sum_distinct"]
     assert st["grid"] == lay.L * lay.N // 64
-    assert st["lds_bytes"] == (lay.n_in + st["n_partial"] + st["n_sum_resident"] + st["segment_slots"] + 1) * 1024 <= 160 * 1024
+    assert st["lds_bytes"] == (lay.n_in + st["n_partial"] + st["n_sum_resident"] + st["segment_slots"] + 1
+                               + st["output_buffer_rows"]) * 1024 <= 160 * 1024
     assert st["waves"] in (8, 16)
+    # outputs in rounds that each fit the output buffer (bursts where outputs are at least
+    # 2.5% of the bytes: VGG11's 6%, not ViT's or BERT's); without bursts, one round stored directly
+    if name == "vgg11":
+        assert st["output_rounds"] == 2 and st["output_buffer_rows"] == 64 and st["waves"] == 16
+        assert st["output_rounds"] * st["output_buffer_rows"] >= lay.n_out - st["split_outputs"]
+    else:
+        assert st["output_rounds"] == 1 and st["output_buffer_rows"] == 0
+    nb = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_NO_OUTPUT_BURSTS).stats()
+    assert nb["output_rounds"] == 1 and nb["output_buffer_rows"] == 0
+    assert nb["lds_bytes"] == st["lds_bytes"] - st["output_buffer_rows"] * 1024
+
+
+def test_output_rounds_split_evenly():
+    """Consecutive outputs go to rounds of at most the free LDS rows; 150 outputs
+    over 64 inputs (95 free rows) make two rounds of 75; 9 free rows force 17."""
+    for n_in, n_out, rounds, rows in ((64, 150, 2, 75), (150, 150, 17, 9)):
+        cfg = synth.LayerConfig("r", N=128, L=1, n_in=n_in, n_out=n_out, T=4, g=1, ternary=0.0)
+        lay = synth.make_layer(cfg, 2, moduli=synth.ntt_primes(128, 1))
+        ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+        st = fiona.Plan.from_layer(ctx, lay, flags=HOST).stats()
+        assert (st["output_rounds"], st["output_buffer_rows"], st["waves"]) == (rounds, rows, 16)
 
 
 def test_partial_sharing_finds_common_terms():
@@ -188,7 +228,8 @@ def test_partial_sharing_finds_common_terms():
     assert st["n_partial"] > 0 and st["partial_levels"] >= 2
     # one Add/Sub forms each common pair; every sum that holds it saves one
     assert st["addsub_partial"] < st["addsub_shared"] <= st["addsub_unshared"]
-    assert st["lds_bytes"] == (lay.n_in + st["n_partial"] + st["n_sum_resident"] + st["segment_slots"] + 1) * 1024
+    assert st["lds_bytes"] == (lay.n_in + st["n_partial"] + st["n_sum_resident"] + st["segment_slots"] + 1
+                               + st["output_buffer_rows"]) * 1024
     off = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_NO_PARTIAL_SHARING).stats()
     assert off["n_partial"] == 0 and off["addsub_partial"] == off["addsub_shared"] == st["addsub_shared"]
     none = fiona.Plan.from_layer(ctx, lay, flags=HOST | fiona.FIONA_PLAN_NO_SHARING).stats()

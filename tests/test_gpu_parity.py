@@ -41,23 +41,35 @@ def _to_dev(a, dtype, dev):
     return torch.from_numpy(np.ascontiguousarray(a).view(dtype)).to(dev)
 
 
-def _run(layer, dev, x=None, pt=None, flags=0, scales=None, signs=None):
-    """Run the layer on the GPU; x/pt from host arrays or, if None, filled on the device."""
+POISON = -1   # all-ones words in the padding between plaintext rows: never a residue
+
+
+def _run(layer, dev, x=None, pt=None, flags=0, scales=None, signs=None, pitch=0):
+    """Run the layer on the GPU; x/pt from host arrays or, if None, filled on the device.
+    pitch: words between plaintext rows (0 = packed L*N, "hint" = fiona_pt_pitch_hint);
+    the padding between rows holds all-ones words."""
     import torch
     import synth.gpu
     N, L = layer.N, layer.L
     ctx = fiona.Ctx(N, L, layer.moduli)
-    plan = fiona.Plan.from_layer(ctx, layer, flags=flags)
+    if pitch == "hint":
+        pitch = ctx.pt_pitch_hint()
+    plan = fiona.Plan.from_layer(ctx, layer, flags=flags, pt_pitch=pitch)
     if x is None:
         in_t = torch.empty(layer.n_in * 2 * L * N, dtype=torch.int64, device=dev)
         synth.gpu.fill_inputs(layer, in_t)
     else:
         in_t = _to_dev(x, np.int64, dev)
+    P = plan.pt_pitch
     if pt is None:
-        pt_t = torch.empty(max(1, layer.n_pt * L * N), dtype=torch.int64, device=dev)
-        synth.gpu.fill_pts(layer, pt_t)
+        pt_t = torch.full((max(1, plan.pt_words()),), POISON, dtype=torch.int64, device=dev)
+        synth.gpu.fill_pts(layer, pt_t, P)
+    elif not pt.size:
+        pt_t = torch.zeros(1, dtype=torch.int64, device=dev)
     else:
-        pt_t = _to_dev(pt, np.int64, dev) if pt.size else torch.zeros(1, dtype=torch.int64, device=dev)
+        padded = np.full((layer.n_pt, P), np.uint64(2**64 - 1), np.uint64)
+        padded[:, : L * N] = np.ascontiguousarray(pt).reshape(layer.n_pt, L * N)
+        pt_t = _to_dev(padded.reshape(-1)[: plan.pt_words()], np.int64, dev)
     sg = layer.mem_sign if signs is None else signs
     sign_t = _to_dev(sg, np.int8, dev) if sg.size else torch.zeros(1, dtype=torch.int8, device=dev)
     sc = layer.scales if scales is None else scales
@@ -95,6 +107,25 @@ SMALL = {
 }
 
 
+def _merge_layers(a, b):
+    """The outputs of a followed by those of b (same ring, moduli, seed and inputs)."""
+    assert (a.N, a.L, a.n_in, a.seed, list(a.moduli)) == (b.N, b.L, b.n_in, b.seed, list(b.moduli))
+    cat = np.concatenate
+    return synth.Layer(
+        cfg=a.cfg, moduli=a.moduli, seed=a.seed, n_in=a.n_in, n_out=a.n_out + b.n_out,
+        out_global=cat([a.out_global, b.out_global + a.n_out]).astype(np.uint32),
+        pm_off=cat([a.pm_off, b.pm_off[1:] + a.pm_off[-1]]).astype(np.uint32),
+        pm_input=cat([a.pm_input, b.pm_input]).astype(np.uint32),
+        pm_pt=cat([a.pm_pt, b.pm_pt + a.n_pt]).astype(np.uint32),
+        grp_off=cat([a.grp_off, b.grp_off[1:] + a.grp_off[-1]]).astype(np.uint32),
+        grp_mem_off=cat([a.grp_mem_off, b.grp_mem_off[1:] + a.grp_mem_off[-1]]).astype(np.uint32),
+        mem_input=cat([a.mem_input, b.mem_input]).astype(np.uint32),
+        mem_sign=cat([a.mem_sign, b.mem_sign]).astype(np.int8),
+        grp_scale=cat([a.grp_scale, b.grp_scale + len(a.scales)]).astype(np.uint32),
+        scales=cat([a.scales, b.scales]).astype(np.uint64),
+        pt_global=cat([a.pt_global, b.pt_global]).astype(np.uint64))
+
+
 def _small_layer(name):
     cfg = SMALL[name]
     if name == "tiny":
@@ -120,13 +151,47 @@ def test_small_layer_elementwise(dev, name):
                                         ("partial_share", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
                                         ("partial_share", fiona.FIONA_PLAN_NO_LDS_SUMS),
                                         ("ragged_pool", fiona.FIONA_PLAN_PER_CONTRIBUTION),
-                                        ("partial_share", fiona.FIONA_PLAN_PER_CONTRIBUTION)])
+                                        ("partial_share", fiona.FIONA_PLAN_PER_CONTRIBUTION),
+                                        ("many_outputs", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
+                                        ("partial_share", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
+                                        ("fold_raw", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS)])
 def test_plan_variants_agree(dev, name, flags):
     layer = _small_layer(name)
     x, pt = synth.input_values(layer), synth.pt_values(layer)
     expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
     out_t, *_ = _run(layer, dev, x, pt, flags=flags)
     _assert_equal(_host(out_t, layer), expect, "flags=%d" % flags)
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged_pool", "fold_raw", "partial_share"])
+def test_padded_plaintext_pitch(dev, name):
+    """Plaintext rows at the library's padded pitch and at an odd pitch (L*N + 1),
+    all-ones words in between: the same exact result, so no padding word is read."""
+    layer = _small_layer(name)
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    for pitch in ("hint", layer.L * layer.N + 1):
+        out_t, *_ = _run(layer, dev, x, pt, pitch=pitch)
+        _assert_equal(_host(out_t, layer), expect, "%s pitch %s" % (name, pitch))
+
+
+@pytest.mark.parametrize("long_first", [True, False])
+def test_output_rounds_with_split_outputs(dev, long_first):
+    """Three rounds of buffered outputs with two long outputs split over
+    wavefronts in the first or the last round (ragged N)."""
+    q = synth.ntt_primes(256, 2)
+    long_ = synth.make_layer(synth.LayerConfig("long", N=192, L=2, n_in=130, n_out=2, T=1500, g=10,
+                                               ternary=0.5), 4, moduli=q)
+    short = synth.make_layer(synth.LayerConfig("short", N=192, L=2, n_in=130, n_out=40, T=20, g=10,
+                                                ternary=0.5), 4, moduli=q)
+    layer = _merge_layers(long_, short) if long_first else _merge_layers(short, long_)
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    st = fiona.Plan.from_layer(ctx, layer, flags=fiona.FIONA_PLAN_HOST_ONLY).stats()
+    assert st["output_rounds"] == 3 and st["split_outputs"] == 2 and st["output_buffer_rows"] > 0, st
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    out_t, *_ = _run(layer, dev, x, pt)
+    _assert_equal(_host(out_t, layer), expect, "rounds, long outputs %s" % ("first" if long_first else "last"))
 
 
 def test_seeds_2_and_3_tiny(dev):
@@ -252,7 +317,7 @@ def test_full_size_sampled(dev, name):
     layer = synth.make_layer(synth.CONFIGS[name], 1)
     _say("[parity] %s full size: %d outputs, %d raw terms, %d groups" % (name, layer.n_out, layer.n_pm,
                                                                         layer.n_group))
-    out_t, in_t, pt_t, plan = _run(layer, dev)
+    out_t, in_t, pt_t, plan = _run(layer, dev, pitch="hint")   # the benchmark's plaintext layout
     _say("[parity] %s kernel done, plan %s" % (name, plan.stats()))
     del pt_t
     _check_sampled(layer, out_t, in_t, 48, 100, name)
@@ -270,14 +335,15 @@ def test_full_size_large_all_chunks(dev):
     x_s = synth.input_values(layer, (limbs, coeffs))
     chunks = synth.output_chunks(layer.n_out, layer.cfg.chunks_hybrid)
     max_pt = max(synth.chunk_layer(layer, a, b).n_pt for a, b in chunks)
-    pt_t = torch.empty(max_pt * layer.L * layer.N, dtype=torch.int64, device=dev)
-    out_c = torch.empty((layer.n_out // len(chunks) + 1) * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
     ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    pitch = ctx.pt_pitch_hint()   # the benchmark's plaintext layout
+    pt_t = torch.empty((max_pt - 1) * pitch + layer.L * layer.N, dtype=torch.int64, device=dev)
+    out_c = torch.empty((layer.n_out // len(chunks) + 1) * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
     sign_all = _to_dev(layer.mem_sign, np.int8, dev)
     for ci, (a, b) in enumerate(chunks):
         ch = synth.chunk_layer(layer, a, b)
-        synth.gpu.fill_pts(ch, pt_t)
-        plan = fiona.Plan.from_layer(ctx, ch)
+        synth.gpu.fill_pts(ch, pt_t, pitch)
+        plan = fiona.Plan.from_layer(ctx, ch, pt_pitch=pitch)
         sign_t = _to_dev(ch.mem_sign, np.int8, dev)
         scale_t = _to_dev(ch.scales, np.int64, dev)
         fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_c)
@@ -297,10 +363,10 @@ def test_full_size_all_pmult_route_equivalence(dev):
     """VGG11-like layer: the all-PMult layer gives exactly the hybrid outputs at every position."""
     import torch
     layer = synth.make_layer(synth.CONFIGS["vgg11"], 1)
-    out_h, in_t, pt_t, _ = _run(layer, dev)
+    out_h, in_t, pt_t, _ = _run(layer, dev, pitch="hint")
     del pt_t
     allpm = synth.all_pmult_layer(layer)
-    out_a, in_a, pt_a, _ = _run(allpm, dev)
+    out_a, in_a, pt_a, _ = _run(allpm, dev, pitch="hint")
     del pt_a, in_a
     assert torch.equal(out_h, out_a)
     _check_sampled(allpm, out_a, in_t, 16, 102, "vgg11 all-PMult")
