@@ -517,12 +517,17 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
       size_t e = t;
       while (e < t1 && e - t < fiona::kChunkTerms && terms[e].first - cbase < (1ull << 31)) ++e;
       const uint32_t n = (uint32_t)(e - t), nb = (n + fiona::kRawBatch - 1) / fiona::kRawBatch;
+      // block: kChunkSlots plaintext offsets, then kChunkSlots input rows (as
+      // kChunkSlots uint2 words); slot kChunkSlots-1 of each half is the header
       const size_t blk = P->pm.size();
       P->pm.resize(blk + fiona::kChunkSlots, make_uint2(0, 0));
-      for (uint32_t r = 0; r < nb * fiona::kRawBatch; ++r)
-        P->pm[blk + r] = r < n ? make_uint2((uint32_t)(terms[t + r].first - cbase), terms[t + r].second * kSlotBytes)
-                               : make_uint2(0, zero_row * kSlotBytes);
-      P->pm[blk + fiona::kChunkSlots - 1] = make_uint2((uint32_t)cbase, (uint32_t)(cbase >> 32) | (nb << 16));
+      uint32_t *w = (uint32_t *)&P->pm[blk];
+      for (uint32_t r = 0; r < nb * fiona::kRawBatch; ++r) {
+        w[r] = r < n ? (uint32_t)(terms[t + r].first - cbase) : 0u;
+        w[fiona::kChunkSlots + r] = (r < n ? terms[t + r].second : zero_row) * kSlotBytes;
+      }
+      w[fiona::kChunkSlots - 1] = (uint32_t)cbase;
+      w[2 * fiona::kChunkSlots - 1] = (uint32_t)(cbase >> 32) | (nb << 16);
       t = e;
     }
     return make_uint2(first, (uint32_t)(P->pm.size() / fiona::kChunkSlots) - first);

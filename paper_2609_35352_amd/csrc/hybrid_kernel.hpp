@@ -20,10 +20,12 @@
 //      and Raw Routes"), reduced once to a canonical residue.  A whole output
 //      is written at once; the segments of a split output leave their
 //      residues in LDS and are added after a barrier.
-// Plan records are wave-uniform: a wavefront loads up to 64 records with one
-// vector load (one per lane), one chunk or item ahead of their use, and
-// broadcasts them into scalar registers with v_readlane, so all control flow
-// is uniform.  No MFMA: this is modular integer arithmetic.
+// Plan records are wave-uniform.  Work items and raw-term records are read
+// with scalar loads straight into SGPRs (every tile reads the same records, so
+// they stay in the scalar cache); the use records and member words of signed
+// sums are loaded one per lane with a vector load and broadcast with
+// v_readlane.  All control flow is uniform.  No MFMA: this is modular integer
+// arithmetic.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -160,38 +162,58 @@ __device__ __forceinline__ uint4 signed_sum(uint32_t wv, const uint4 *lds, uint3
                     (uint32_t)pb - (uint32_t)nb, (uint32_t)(pb >> 32) - (uint32_t)(nb >> 32));
 }
 
-// Raw-term chunks.  A chunk is a block of kChunkSlots records (one per lane):
-// record r < 8 nb is {byte offset of the term's plaintext from the chunk
-// base, LDS byte offset of the term's input row}; padding records point at
-// offset 0 and the all-zero row, so they add nothing.  The header record (the
-// last lane) is {chunk base bits 0..31, bits 32..47 | nb << 16}; the chunk
-// base is a byte offset into the plaintext table.  The plaintext of record r
-// is read with a buffer load: descriptor base = this tile's plaintext column
-// at the chunk base, and lane offset plus record offset in one VGPR (an
-// SGPR offset that changes from load to load streams measurably slower).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const char *pt_tile, uint2 rec, uint32_t &nb) {
-  const uint32_t lo = bcast(rec.x, kChunkSlots - 1), hi = bcast(rec.y, kChunkSlots - 1);
-  nb = hi >> 16;
-  const char *base = pt_tile + pair64(lo, hi & 0xFFFFu);
-  return __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)0xFFFFFFFF, 0x00020000);
+// Scalar (SMEM) loads of plan records.  Every wavefront of every tile reads
+// the same records, so they come from the scalar cache straight into SGPRs:
+// no vector load and no v_readlane per record.  The address must be uniform.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+typedef const __attribute__((address_space(4))) uint32_t *cu32p;
+typedef const __attribute__((address_space(4))) u32x2 *cu32x2p;
+typedef const __attribute__((address_space(4))) u32x4 *cu32x4p;
+typedef const __attribute__((address_space(4))) u32x16 *cu32x16p;
+__device__ __forceinline__ uint32_t sload1(const void *p) { return *(cu32p)p; }
+__device__ __forceinline__ u32x2 sload2(const void *p) { return *(cu32x2p)p; }
+__device__ __forceinline__ u32x4 sload4(const void *p) { return *(cu32x4p)p; }
+__device__ __forceinline__ u32x16 sload16(const void *p) { return *(cu32x16p)p; }
+__device__ __forceinline__ uint4 as_uint4(u32x4 v) { return make_uint4(v.x, v.y, v.z, v.w); }
+__device__ __forceinline__ uint2 as_uint2(u32x2 v) { return make_uint2(v.x, v.y); }
+
+typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+typedef const __attribute__((address_space(4))) u32x8 *cu32x8p;
+__device__ __forceinline__ u32x8 sload8(const void *p) { return *(cu32x8p)p; }
+
+// Raw-term chunks.  A chunk block holds kChunkSlots plaintext offsets, then
+// kChunkSlots input rows; record r < 8 nb is (offset r, row r): the byte
+// offset of the term's plaintext from the chunk base and the LDS byte offset
+// of its input row.  Padding records point at offset 0 and the all-zero row,
+// so they add nothing.  Slot kChunkSlots-1 of the two halves is the header:
+// chunk base bits 0..31, and bits 32..47 | nb << 16; the chunk base is a byte
+// offset into the plaintext table.  A plaintext is read with a buffer load:
+// descriptor base = this tile's plaintext column at the chunk base, and lane
+// offset plus record offset in the VGPR offset (an SGPR offset that changes
+// from load to load streamed measurably slower).  A batch's offsets and rows
+// are loaded separately, so only the offsets of the batch about to be issued
+// and the rows of the batch being multiplied occupy SGPRs.
+__device__ __forceinline__ u32x8 batch_offsets(const uint32_t *blk, uint32_t b) { return sload8(blk + b * kRawBatch); }
+__device__ __forceinline__ u32x8 batch_rows(const uint32_t *blk, uint32_t b) {
+  return sload8(blk + kChunkSlots + b * kRawBatch);
 }
 
-// Issue the plaintext loads of the batch of records r0 .. r0+7 of a chunk.
-__device__ __forceinline__ void raw_issue(u32x2 (&w)[kRawBatch], __amdgpu_buffer_rsrc_t rs, uint2 rec, uint32_t r0,
-                                          uint32_t voff) {
+// Issue the plaintext loads of one batch, offsets in SGPRs.
+__device__ __forceinline__ void raw_issue_s(u32x2 (&w)[kRawBatch], __amdgpu_buffer_rsrc_t rs, u32x8 off,
+                                            uint32_t voff) {
 #pragma unroll
-  for (uint32_t u = 0; u < kRawBatch; ++u)
-    w[u] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + bcast(rec.x, r0 + u), 0, kLoadNT);
+  for (uint32_t u = 0; u < kRawBatch; ++u) w[u] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + off[u], 0, kLoadNT);
 }
 
-// Multiply-accumulate the batch of records r0 .. r0+7, whose plaintext words are in w.
-__device__ __forceinline__ void raw_consume(Acc &a0, Acc &a1, const u32x2 (&w)[kRawBatch], uint2 rec, uint32_t r0,
-                                            const uint4 *lds, uint32_t lane16) {
+// Multiply-accumulate one batch whose plaintext words are in w, input rows in SGPRs.
+__device__ __forceinline__ void raw_consume_s(Acc &a0, Acc &a1, const u32x2 (&w)[kRawBatch], u32x8 row,
+                                              const uint4 *lds, uint32_t lane16) {
 #pragma unroll
   for (uint32_t h = 0; h < kRawBatch; h += 4) {
     uint4 x[4];
 #pragma unroll
-    for (uint32_t u = 0; u < 4; ++u) x[u] = lds_row(lds, bcast(rec.y, r0 + h + u), lane16);
+    for (uint32_t u = 0; u < 4; ++u) x[u] = lds_row(lds, row[h + u], lane16);
 #pragma unroll
     for (uint32_t u = 0; u < 4; ++u) {
       mac(a0, x[u].x, x[u].y, w[h + u].x, w[h + u].y);
@@ -200,26 +222,33 @@ __device__ __forceinline__ void raw_consume(Acc &a0, Acc &a1, const u32x2 (&w)[k
   }
 }
 
-// All nb batches of a chunk: a software pipeline that keeps batch b+1 in
-// flight while batch b is multiplied.  The steady state issues the same
-// loads on every path, so the wait counts stay exact.
-__device__ __forceinline__ void raw_chunk(uint32_t nb, __amdgpu_buffer_rsrc_t rs, uint2 rec, uint32_t voff, Acc &a0,
-                                          Acc &a1, const uint4 *lds, uint32_t lane16) {
+__device__ __forceinline__ const uint32_t *sload_block(const uint2 *pm, uint32_t chunk) {
+  return (const uint32_t *)(pm + (size_t)chunk * kChunkSlots);
+}
+
+// All batches of the chunk block blk (uniform address), records in SGPRs:
+// batch b+1 is in flight while batch b is multiplied.
+__device__ __forceinline__ void raw_chunk(const uint32_t *blk, const char *pt_tile, uint32_t voff, Acc &a0, Acc &a1,
+                                          const uint4 *lds, uint32_t lane16) {
+  const uint32_t hlo = sload1(blk + kChunkSlots - 1), hhi = sload1(blk + 2 * kChunkSlots - 1);
+  const uint32_t nb = hhi >> 16;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(pt_tile + pair64(hlo, hhi & 0xFFFFu)), (short)0, (int)0xFFFFFFFF, 0x00020000);
   u32x2 wa[kRawBatch], wb[kRawBatch];
-  raw_issue(wa, rs, rec, 0, voff);
+  raw_issue_s(wa, rs, batch_offsets(blk, 0), voff);
   uint32_t b = 0;
   for (; b + 2 < nb; b += 2) {   // batch b is in flight in wa
-    raw_issue(wb, rs, rec, (b + 1) * kRawBatch, voff);
-    raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
-    raw_issue(wa, rs, rec, (b + 2) * kRawBatch, voff);
-    raw_consume(a0, a1, wb, rec, (b + 1) * kRawBatch, lds, lane16);
+    raw_issue_s(wb, rs, batch_offsets(blk, b + 1), voff);
+    raw_consume_s(a0, a1, wa, batch_rows(blk, b), lds, lane16);
+    raw_issue_s(wa, rs, batch_offsets(blk, b + 2), voff);
+    raw_consume_s(a0, a1, wb, batch_rows(blk, b + 1), lds, lane16);
   }
   if (b + 1 < nb) {   // two batches left, the first in flight in wa
-    raw_issue(wb, rs, rec, (b + 1) * kRawBatch, voff);
-    raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
-    raw_consume(a0, a1, wb, rec, (b + 1) * kRawBatch, lds, lane16);
+    raw_issue_s(wb, rs, batch_offsets(blk, b + 1), voff);
+    raw_consume_s(a0, a1, wa, batch_rows(blk, b), lds, lane16);
+    raw_consume_s(a0, a1, wb, batch_rows(blk, b + 1), lds, lane16);
   } else {
-    raw_consume(a0, a1, wa, rec, b * kRawBatch, lds, lane16);
+    raw_consume_s(a0, a1, wa, batch_rows(blk, b), lds, lane16);
   }
 }
 
@@ -242,9 +271,6 @@ __device__ __forceinline__ void fold(Acc &a0, Acc &a1, uint64_t &r0, uint64_t &r
   acc_zero(a1);
 }
 
-__device__ __forceinline__ uint2 load_chunk(const uint2 *pm, uint32_t chunk, uint32_t lane) {
-  return pm[(size_t)chunk * kChunkSlots + lane];
-}
 __device__ __forceinline__ uint4 load_use_chunk(const uint4 *uses, uint32_t begin, uint32_t count, uint32_t lane) {
   return lane < count ? uses[begin + lane] : make_uint4(0, kInlineSum, 0, 0);
 }
@@ -329,17 +355,14 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
   const uint32_t voff = lane_off * 8u;
   const uint32_t out_row = limb * S.N + k0;   // offset of this tile in one output polynomial
   for (uint32_t rd = 0; rd < S.n_rounds; ++rd) {
-  const uint2 wr = K.waves[rd * NW + wave];
-  uint4 item_next = wr.y ? items[wr.x] : make_uint4(0, 0, 0, 0);
-  uint2 raw_next = item_next.y ? load_chunk(pm, item_next.x, lane) : make_uint2(0, 0);
+  const uint2 wr = as_uint2(sload2(K.waves + rd * NW + wave));
+  uint4 item_next = wr.y ? as_uint4(sload4(items + wr.x)) : make_uint4(0, 0, 0, 0);
   uint4 use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
   for (uint32_t it = wr.x; it < wr.x + wr.y; ++it) {
     const uint4 item = item_next;   // first chunk, chunks, first use, uses
-    uint2 raw_rec = raw_next;
     uint4 use_rec = use_next;
     if (it + 1 < wr.x + wr.y) {
-      item_next = items[it + 1];
-      raw_next = item_next.y ? load_chunk(pm, item_next.x, lane) : make_uint2(0, 0);
+      item_next = as_uint4(sload4(items + it + 1));
       use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
     }
     // word blocks of this item's first two uses (loaded before the raw route,
@@ -357,15 +380,11 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
     // raw route: one PMult per term, chunk by chunk; within a chunk batch b+1
     // is in flight while batch b is multiplied
     for (uint32_t c = 0; c < item.y; ++c) {
-      const uint2 rec = raw_rec;
-      if (c + 1 < item.y) raw_rec = load_chunk(pm, item.x + c + 1, lane);
       if (c) {
         if (c % kFoldChunks == 0) fold(a0, a1, r0, r1, lc);   // keep the accumulators exact
         else { carry(a0); carry(a1); }
       }
-      uint32_t nb;
-      const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(pt_tile, rec, nb);
-      raw_chunk(nb, rs, rec, voff, a0, a1, lds, lane16);
+      raw_chunk(sload_block(pm, item.x + c), pt_tile, voff, a0, a1, lds, lane16);
     }
 
     // signed route: each use applies its group's scale once to a signed sum.
@@ -403,7 +422,7 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
 
     const uint64_t y0 = finish(a0, r0, lc);
     const uint64_t y1 = finish(a1, r1, lc);
-    const uint32_t d = dest[it];
+    const uint32_t d = sload1(dest + it);
     if (d & kSegmentFlag) {
       segs[(d & ~kSegmentFlag) * kTile + lane] =
           make_uint4((uint32_t)y0, (uint32_t)(y0 >> 32), (uint32_t)y1, (uint32_t)(y1 >> 32));
