@@ -78,18 +78,16 @@ struct fiona_plan {
   uint32_t n_rounds = 1, obuf_rows = 0;
   uint32_t nw = 8, n_seg_slots = 0;
   std::vector<uint2> pm;
-  std::vector<uint4> uses;
-  std::vector<uint32_t> mats;
+  uint32_t n_uses = 0;
   std::vector<uint2> members;
-  std::vector<uint2> sums_dev;
+  std::vector<uint4> blocks;   // word blocks: common partial sums, resident sums, uses (see PackParams)
   void *dev = nullptr;
   int device = -1;
   // device pointers into dev
   const LimbConst *d_limbs = nullptr;
-  const uint4 *d_items = nullptr, *d_splits = nullptr, *d_uses = nullptr, *d_rounds = nullptr;
+  const uint4 *d_items = nullptr, *d_splits = nullptr, *d_rounds = nullptr, *d_blocks = nullptr;
   const uint32_t *d_dest = nullptr, *d_flush = nullptr;
-  const uint2 *d_waves = nullptr, *d_pm = nullptr, *d_members = nullptr, *d_sums = nullptr;
-  const uint32_t *d_mats = nullptr;
+  const uint2 *d_waves = nullptr, *d_pm = nullptr, *d_members = nullptr;
   uint32_t *d_words = nullptr;
   KShape shape{};
   uint32_t lds_bytes = 0, grid = 0, tiles = 0;
@@ -192,7 +190,7 @@ struct SumBuild {
   bool flip = false;                // representative's canonicalisation flipped its signs
   uint32_t n_use = 0;
   uint32_t slot = fiona::kInlineSum;
-  uint32_t word_begin = 0;          // header word, then the member words
+  uint32_t member_begin = 0;        // its members in the device member list
 };
 
 // A common partial sum: first + rel * second (rows as in MemberRef).  Its two
@@ -447,19 +445,18 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
     }
   }
 
-  // Device records.  Words: one block per common partial sum, then one per
-  // distinct signed sum; the sign-packing kernel fills them on every call.
+  // Device records.  Word blocks: one per common partial sum, one per resident
+  // signed sum, then one per use; the sign-packing kernel fills them on every
+  // call.  Block = {member begin, count | flags, resident slot, scale | negate}.
   for (uint32_t p = 0; p < n_part; ++p) {
     const uint32_t mb = (uint32_t)P->members.size();
     P->members.push_back(make_uint2(parts[p].first.row, parts[p].first.slot));
     P->members.push_back(make_uint2(parts[p].second.row, parts[p].second.slot));
-    P->sums_dev.push_back(make_uint2(mb, 2u | fiona::kNormaliseSigns));
+    P->blocks.push_back(make_uint4(mb, 2u | fiona::kNormaliseSigns, fiona::kInlineSum, 0));
   }
   for (auto &sb : sums) {
-    const uint32_t mb = (uint32_t)P->members.size();
-    sb.word_begin = (uint32_t)P->sums_dev.size() * fiona::kSumWords;
+    sb.member_begin = (uint32_t)P->members.size();
     for (auto &m : sb.members) P->members.push_back(make_uint2(m.row, m.slot));
-    P->sums_dev.push_back(make_uint2(mb, (uint32_t)sb.members.size()));
   }
   // Rows of common terms are numbered level by level (a term only reads rows
   // of lower levels), so each level is formed after a barrier; part_levels[l]
@@ -475,8 +472,8 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
     for (uint32_t t = 0; t < n_part; ++t) new_row[order[t]] = t;
     for (auto &m : P->members)
       if (m.x >= d->n_in) m.x = d->n_in + new_row[m.x - d->n_in];
-    const std::vector<uint2> blocks(P->sums_dev.begin(), P->sums_dev.begin() + n_part);
-    for (uint32_t p = 0; p < n_part; ++p) P->sums_dev[new_row[p]] = blocks[p];
+    const std::vector<uint4> blocks(P->blocks.begin(), P->blocks.begin() + n_part);
+    for (uint32_t p = 0; p < n_part; ++p) P->blocks[new_row[p]] = blocks[p];
     P->part_levels.assign(kMaxPartialLevels, 0);
     for (uint32_t t = 0; t < n_part; ++t) {
       const uint32_t lv = parts[order[t]].level;
@@ -486,16 +483,21 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   }
   P->n_levels = n_levels;
   for (uint32_t s : cand) {
-    sums[s].slot = (uint32_t)P->mats.size();
-    P->mats.push_back(sums[s].word_begin);
+    sums[s].slot = P->n_mat++;
+    P->blocks.push_back(make_uint4(sums[s].member_begin, (uint32_t)sums[s].members.size(), fiona::kInlineSum, 0));
   }
-  P->n_mat = (uint32_t)P->mats.size();
   std::vector<uint32_t> use_begin(d->n_out);
   for (uint32_t j = 0; j < d->n_out; ++j) {
-    use_begin[j] = (uint32_t)P->uses.size();
+    use_begin[j] = P->n_uses;
     for (const Use &u : out_uses[j]) {
       const SumBuild &sb = sums[u.sum];
-      P->uses.push_back(make_uint4(sb.word_begin, sb.slot, u.scale | (u.neg ? 0x80000000u : 0u), 0));
+      const uint32_t sc = u.scale | (u.neg ? 0x80000000u : 0u);
+      if (sb.slot != fiona::kInlineSum)   // a resident sum: no members, its LDS slot
+        P->blocks.push_back(make_uint4(0, fiona::kUseBlock, sb.slot, sc));
+      else
+        P->blocks.push_back(make_uint4(sb.member_begin, (uint32_t)sb.members.size() | fiona::kUseBlock,
+                                       fiona::kInlineSum, sc));
+      P->n_uses++;
     }
   }
   P->st.addsub_partial = addsub_partial;
@@ -507,7 +509,7 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   // terms of an output may be taken in any order (the sum is exact), so they
   // are sorted by plaintext offset: a chunk then covers a short stretch of the
   // plaintext table, and its terms' offsets from the chunk base fit 31 bits.
-  const uint32_t zero_row = d->n_in + n_part + (uint32_t)P->mats.size() + seg_slots;
+  const uint32_t zero_row = d->n_in + n_part + P->n_mat + seg_slots;
   const uint64_t ln8 = P->pt_pitch * 8;
   auto emit_chunks = [&](const std::vector<std::pair<uint64_t, uint32_t>> &terms, size_t t0, size_t t1) {
     const uint32_t first = (uint32_t)(P->pm.size() / fiona::kChunkSlots);
@@ -614,14 +616,14 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   st.n_member = P->n_member_desc;
   st.ct_terms = (uint64_t)n_pm + P->n_member_desc;
   st.n_member_nonzero = nz_members;
-  st.n_use = P->uses.size();
+  st.n_use = P->n_uses;
   st.n_sum_distinct = sums.size();
   st.n_sum_resident = P->n_mat;
   st.pmult_per_contribution = (uint64_t)n_pm + nz_members;
-  st.pmult_grouped = (uint64_t)n_pm + P->uses.size();
+  st.pmult_grouped = (uint64_t)n_pm + P->n_uses;
   st.addsub_unshared = addsub_unshared;
   st.addsub_shared = addsub_shared;
-  P->any_signed = !P->uses.empty();
+  P->any_signed = P->n_uses > 0;
   return FIONA_OK;
 }
 
@@ -636,12 +638,10 @@ int upload_plan(fiona_plan *P) {
   const size_t o_rounds = align_up(o_splits + sizeof(uint4) * P->splits.size(), a);
   const size_t o_flush = align_up(o_rounds + sizeof(uint4) * P->rounds.size(), a);
   const size_t o_pm = align_up(o_flush + sizeof(uint32_t) * P->flush.size(), a);
-  const size_t o_uses = align_up(o_pm + sizeof(uint2) * P->pm.size(), a);
-  const size_t o_mats = align_up(o_uses + sizeof(uint4) * P->uses.size(), a);
-  const size_t o_mem = align_up(o_mats + sizeof(uint32_t) * P->mats.size(), a);
-  const size_t o_sums = align_up(o_mem + sizeof(uint2) * P->members.size(), a);
-  const size_t o_words = align_up(o_sums + sizeof(uint2) * P->sums_dev.size(), a);
-  const size_t n_words = P->sums_dev.size() * fiona::kSumWords;
+  const size_t o_mem = align_up(o_pm + sizeof(uint2) * P->pm.size(), a);
+  const size_t o_blocks = align_up(o_mem + sizeof(uint2) * P->members.size(), a);
+  const size_t o_words = align_up(o_blocks + sizeof(uint4) * P->blocks.size(), a);
+  const size_t n_words = P->blocks.size() * fiona::kSumWords;
   const size_t total = align_up(o_words + sizeof(uint32_t) * n_words, a);
   std::vector<unsigned char> host(total, 0);
   auto put = [&](size_t off, const void *src, size_t n) { if (n) std::memcpy(host.data() + off, src, n); };
@@ -653,10 +653,8 @@ int upload_plan(fiona_plan *P) {
   put(o_rounds, P->rounds.data(), sizeof(uint4) * P->rounds.size());
   put(o_flush, P->flush.data(), sizeof(uint32_t) * P->flush.size());
   put(o_pm, P->pm.data(), sizeof(uint2) * P->pm.size());
-  put(o_uses, P->uses.data(), sizeof(uint4) * P->uses.size());
-  put(o_mats, P->mats.data(), sizeof(uint32_t) * P->mats.size());
   put(o_mem, P->members.data(), sizeof(uint2) * P->members.size());
-  put(o_sums, P->sums_dev.data(), sizeof(uint2) * P->sums_dev.size());
+  put(o_blocks, P->blocks.data(), sizeof(uint4) * P->blocks.size());
   if (hipGetDevice(&P->device) != hipSuccess) return FIONA_ERR_HIP;
   if (hipMalloc(&P->dev, total) != hipSuccess) {
     P->dev = nullptr;
@@ -681,10 +679,8 @@ int upload_plan(fiona_plan *P) {
   P->d_rounds = (const uint4 *)(base + o_rounds);
   P->d_flush = (const uint32_t *)(base + o_flush);
   P->d_pm = (const uint2 *)(base + o_pm);
-  P->d_uses = (const uint4 *)(base + o_uses);
-  P->d_mats = (const uint32_t *)(base + o_mats);
   P->d_members = (const uint2 *)(base + o_mem);
-  P->d_sums = (const uint2 *)(base + o_sums);
+  P->d_blocks = (const uint4 *)(base + o_blocks);
   P->d_words = (uint32_t *)(base + o_words);
   return FIONA_OK;
 }
@@ -742,6 +738,7 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   k.zero_row = P->n_in + P->n_part + P->n_mat + P->n_seg_slots;
   k.n_rounds = P->n_rounds;
   k.obuf_row = k.zero_row + 1;
+  k.use_block0 = P->n_part + P->n_mat;
   k.n_part = P->n_part;
   k.n_levels = P->n_levels;
   for (uint32_t l = 0; l < fiona::kMaxLevels; ++l) k.level_end[l] = P->part_levels[l];
@@ -795,22 +792,17 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   if (plan->n_out == 0) return FIONA_OK;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return FIONA_ERR_ARG;
-  const uint32_t n_sums = (uint32_t)plan->sums_dev.size();
-  const uint32_t n_uses = (uint32_t)plan->uses.size();
-  if (n_sums) {   // this call's signs and scales: the word blocks and the uses' signed scales
+  const uint32_t n_blocks = (uint32_t)plan->blocks.size();
+  if (n_blocks) {   // this call's signs and scales: the word blocks
     PackParams pp;
     pp.signs = ternary_groups;
     pp.members = plan->d_members;
-    pp.sums = plan->d_sums;
+    pp.blocks = plan->d_blocks;
     pp.words = plan->d_words;
     pp.scales = scales;
-    pp.uses = const_cast<uint4 *>(plan->d_uses);
-    pp.n_sums = n_sums;
+    pp.n_blocks = n_blocks;
     pp.zero_row = plan->shape.zero_row;
-    pp.n_uses = n_uses;
-    pp.sum_blocks = (n_sums + 3) / 4;
-    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3(pp.sum_blocks + (n_uses + 255) / 256), dim3(256), 0, stream,
-                       pp);
+    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((n_blocks + 3) / 4), dim3(256), 0, stream, pp);
     if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   }
   auto kernel = plan->nw == 16 ? fiona::hybrid_linear_kernel<16> : fiona::hybrid_linear_kernel<8>;
@@ -823,8 +815,6 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   kp.flush = plan->d_flush;
   kp.splits = plan->d_splits;
   kp.pm = plan->d_pm;
-  kp.uses = plan->d_uses;
-  kp.mats = plan->d_mats;
   kp.words = plan->d_words;
   hipLaunchKernelGGL(kernel, dim3(plan->grid), dim3(plan->nw * 64), plan->lds_bytes, stream, in_cts, pt_diags,
                      out_cts, kp, plan->shape);

@@ -42,7 +42,9 @@ constexpr uint32_t kRawBatches = kChunkTerms / kRawBatch;   // batches per chunk
 constexpr uint32_t kChunkSlots = 64;      // records per chunk block; the last one is the header
 constexpr uint32_t kSumBatch = 4;         // member reads issued before their additions
 constexpr uint32_t kSumBatches = kMaxMembers / kSumBatch;
-constexpr uint32_t kSumWords = 64;        // words per distinct sum: header + padded member rows
+constexpr uint32_t kSumWords = 64;        // words per block: 4 header words + padded member rows
+constexpr uint32_t kAddWord = 4;          // first word of the rows to add
+constexpr uint32_t kUseBlock = 0x40000000u;   // block flag: a use (its header carries a slot and a signed scale)
 constexpr uint32_t kSegmentFlag = 0x80000000u;   // item destination: a segment slot in LDS
 constexpr uint32_t kBufferFlag = 0x40000000u;    // item destination: a row of the output buffer in LDS
 constexpr uint32_t kNormaliseSigns = 0x80000000u;   // block flag: signs relative to the first member's
@@ -50,20 +52,22 @@ constexpr uint32_t kMaxLevels = 4;        // levels of common partial sums
 constexpr int kLoadNT = 2;                // cache policy of the plaintext stream: nontemporal
 constexpr int kStoreNT = 2;               // cache policy of the output stores: nontemporal
 static_assert(kChunkTerms % kRawBatch == 0 && kChunkTerms < kChunkSlots, "chunk layout");
-// header, rows to add from word 1 up, rows to subtract from word 62 down, each list padded to a batch
-static_assert(1 + kMaxMembers + 2 * (kSumBatch - 1) <= kSumWords - 1, "sum block layout");
+// header, rows to add from word 4 up, rows to subtract from word 63 down, each list padded to a batch
+static_assert(kAddWord + kMaxMembers + 2 * (kSumBatch - 1) <= kSumWords, "sum block layout");
+static_assert(kAddWord % kSumBatch == 0 && kSumWords % kSumBatch == 0, "member batches are 16-byte aligned");
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// Per-call description for the sign-packing kernel.
+// Per-call description for the sign-packing kernel.  Word blocks: the common
+// partial sums, the resident signed sums, then one block per use.
 struct PackParams {
   const int8_t *signs;      // [n_member of the layer description]
   const uint2 *members;     // per member: LDS row, index into signs
-  const uint2 *sums;        // per block: member begin, member count (<= kMaxMembers) | kNormaliseSigns
+  const uint4 *blocks;      // per block: member begin, member count (<= kMaxMembers) | kNormaliseSigns |
+                            // kUseBlock, resident slot or kInlineSum, scale index | negate << 31
   uint32_t *words;          // per block: kSumWords words
   const uint64_t *scales;   // [n_scale of the layer description]
-  uint4 *uses;              // per use: .w receives the signed scale of this call
-  uint32_t n_sums, zero_row, n_uses, sum_blocks;
+  uint32_t n_blocks, zero_row;
 };
 
 // Scalars of the main kernel.  LDS rows: inputs, common partial sums (level by
@@ -72,41 +76,32 @@ struct PackParams {
 // produced in n_rounds rounds; each round ends with a barrier after which the
 // round's buffered outputs and split outputs are written out together.
 struct KShape {
-  uint32_t N, L, n_in, n_part, n_levels, n_mat, zero_row, tiles, n_rounds, obuf_row;
+  uint32_t N, L, n_in, n_part, n_levels, n_mat, zero_row, tiles, n_rounds, obuf_row, use_block0;
   uint32_t level_end[kMaxLevels];
 };
 
 __device__ __forceinline__ uint64_t pair64(uint32_t lo, uint32_t hi) { return ((uint64_t)hi << 32) | lo; }
 __device__ __forceinline__ uint32_t pad_batch(uint32_t n) { return (n + kSumBatch - 1) & ~(kSumBatch - 1); }
-__device__ __forceinline__ uint32_t bcast(uint32_t v, uint32_t l) { return __builtin_amdgcn_readlane(v, l); }
 
-// The words of every common partial sum and distinct signed sum for this
-// call.  Word 0 holds the numbers of rows to add and to subtract, each
-// rounded up to a batch of kSumBatch; the rows to add follow from word 1 upwards and
-// the rows to subtract from word 62 downwards, each list padded with the
-// all-zero row.  A row is given as its LDS byte offset.  Members whose
-// run-time sign is 0 are left out (Sec. 3 Obs. 2, the skip).  A common
+// The word blocks of this call.  Word 0 holds the numbers of rows to add and
+// to subtract, each rounded up to a batch of kSumBatch; word 1 the LDS slot
+// of a resident sum (a use of it) or kInlineSum; word 2 a use's signed scale
+// (-1)^negate * c (c < 2^20); word 3 is 0.  The rows to add follow from word
+// 4 upwards and the rows to subtract from word 63 downwards, each list padded
+// with the all-zero row; a row is given as its LDS byte offset.  Members
+// whose run-time sign is 0 are left out (Sec. 3 Obs. 2, the skip).  A common
 // partial sum takes its signs relative to its first member's, so it is the
 // same term in every sum that contains it.  One wavefront per block.
 __global__ void __launch_bounds__(256) pack_members_kernel(const PackParams P) {
-  if (blockIdx.x >= P.sum_blocks) {   // the signed scale of every use: (-1)^negate * c, c < 2^20
-    const uint32_t u = (blockIdx.x - P.sum_blocks) * 256 + threadIdx.x;
-    if (u < P.n_uses) {
-      const uint32_t z = P.uses[u].z;
-      const int32_t c = (int32_t)P.scales[z & 0x7FFFFFFFu];
-      P.uses[u].w = (uint32_t)((z >> 31) ? -c : c);
-    }
-    return;
-  }
   const uint32_t lane = threadIdx.x & 63u;
-  const uint32_t s = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (s >= P.n_sums) return;
-  const uint2 sm = P.sums[s];
-  const uint32_t cnt = sm.y & ~kNormaliseSigns;
-  const int32_t h0 = (sm.y & kNormaliseSigns) ? (int32_t)P.signs[P.members[sm.x].y] : 1;
+  const uint32_t b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= P.n_blocks) return;
+  const uint4 bk = P.blocks[b];
+  const uint32_t cnt = bk.y & 0xFFFFu;
+  const int32_t h0 = (bk.y & kNormaliseSigns) ? (int32_t)P.signs[P.members[bk.x].y] : 1;
   uint32_t cls = 3, row = 0;
   if (lane < cnt) {
-    const uint2 m = P.members[sm.x + lane];
+    const uint2 m = P.members[bk.x + lane];
     const int32_t h = P.signs[m.y] * h0;
     cls = h > 0 ? 0u : (h < 0 ? 1u : 2u);
     row = m.x;
@@ -114,25 +109,50 @@ __global__ void __launch_bounds__(256) pack_members_kernel(const PackParams P) {
   const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
   const uint64_t b0 = __ballot(cls == 0), b1 = __ballot(cls == 1);
   const uint32_t n0 = __popcll(b0), n1 = __popcll(b1), p0 = pad_batch(n0), p1 = pad_batch(n1);
-  uint32_t *w = P.words + (size_t)s * kSumWords;
-  if (cls == 0) w[1 + __popcll(b0 & below)] = row * kRowBytes;
-  if (cls == 1) w[62 - __popcll(b1 & below)] = row * kRowBytes;
+  uint32_t *w = P.words + (size_t)b * kSumWords;
+  if (cls == 0) w[kAddWord + __popcll(b0 & below)] = row * kRowBytes;
+  if (cls == 1) w[kSumWords - 1 - __popcll(b1 & below)] = row * kRowBytes;
   const uint32_t zero = P.zero_row * kRowBytes;
-  if (lane >= 1 + n0 && lane < 1 + p0) w[lane] = zero;
-  if (lane + n1 <= 62 && lane + p1 > 62) w[lane] = zero;
+  if (lane >= kAddWord + n0 && lane < kAddWord + p0) w[lane] = zero;
+  if (lane >= kSumWords - p1 && lane < kSumWords - n1) w[lane] = zero;
   if (lane == 0) w[0] = p0 | (p1 << 16);
+  if (lane == 1) w[1] = bk.z;
+  if (lane == 2) {
+    int32_t sc = 0;
+    if (bk.y & kUseBlock) {
+      const int32_t c = (int32_t)P.scales[bk.w & 0x7FFFFFFFu];
+      sc = (bk.w >> 31) ? -c : c;
+    }
+    w[2] = (uint32_t)sc;
+  }
+  if (lane == 3) w[3] = 0;
 }
 
 __device__ __forceinline__ const uint4 &lds_row(const uint4 *lds, uint32_t row_bytes, uint32_t lane_bytes) {
   return *(const uint4 *)((const char *)lds + row_bytes + lane_bytes);
 }
 
-// Adds the rows at word lanes first + step * u (u < kSumBatch) into the packed digit sums.
-template <int First, int Step>
-__device__ __forceinline__ void sum_batch(uint64_t &a, uint64_t &b, uint32_t wv, const uint4 *lds, uint32_t lane16) {
+// Scalar (SMEM) loads of plan records.  Every wavefront of every tile reads
+// the same records, so they come from the scalar cache straight into SGPRs:
+// no vector load and no v_readlane per record.  The address must be uniform.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+typedef const __attribute__((address_space(4))) uint32_t *cu32p;
+typedef const __attribute__((address_space(4))) u32x2 *cu32x2p;
+typedef const __attribute__((address_space(4))) u32x4 *cu32x4p;
+typedef const __attribute__((address_space(4))) u32x8 *cu32x8p;
+__device__ __forceinline__ uint32_t sload1(const void *p) { return *(cu32p)p; }
+__device__ __forceinline__ u32x2 sload2(const void *p) { return *(cu32x2p)p; }
+__device__ __forceinline__ u32x4 sload4(const void *p) { return *(cu32x4p)p; }
+__device__ __forceinline__ u32x8 sload8(const void *p) { return *(cu32x8p)p; }
+__device__ __forceinline__ uint4 as_uint4(u32x4 v) { return make_uint4(v.x, v.y, v.z, v.w); }
+__device__ __forceinline__ uint2 as_uint2(u32x2 v) { return make_uint2(v.x, v.y); }
+
+// Adds the kSumBatch rows whose LDS byte offsets are in r into the packed digit sums.
+__device__ __forceinline__ void sum_batch(uint64_t &a, uint64_t &b, u32x4 r, const uint4 *lds, uint32_t lane16) {
   uint4 x[kSumBatch];
 #pragma unroll
-  for (int u = 0; u < (int)kSumBatch; ++u) x[u] = lds_row(lds, bcast(wv, First + Step * u), lane16);
+  for (int u = 0; u < (int)kSumBatch; ++u) x[u] = lds_row(lds, r[u], lane16);
 #pragma unroll
   for (int u = 0; u < (int)kSumBatch; ++u) {
     a += pair64(x[u].x, x[u].y);
@@ -140,47 +160,22 @@ __device__ __forceinline__ void sum_batch(uint64_t &a, uint64_t &b, uint32_t wv,
   }
 }
 
-template <int K>
-__device__ __forceinline__ void sum_rows(uint32_t np, uint32_t nn, uint64_t &pa, uint64_t &pb, uint64_t &na,
-                                         uint64_t &nb, uint32_t wv, const uint4 *lds, uint32_t lane16) {
-  if constexpr (K < (int)kSumBatches) {
-    if (K * kSumBatch < np) sum_batch<1 + K * kSumBatch, 1>(pa, pb, wv, lds, lane16);
-    if (K * kSumBatch < nn) sum_batch<62 - K * kSumBatch, -1>(na, nb, wv, lds, lane16);
-    sum_rows<K + 1>(np, nn, pa, pb, na, nb, wv, lds, lane16);
-  }
-}
-
-// Signed sum U = sum h x of one distinct sum whose words are in wv (one per
-// lane), digit-wise: (U0, U1) for each polynomial.  The two 25-bit digits of
-// an input are added as one 64-bit word (the halves never carry into each
-// other for at most 48 members), in batches of kSumBatch LDS reads.
-__device__ __forceinline__ uint4 signed_sum(uint32_t wv, const uint4 *lds, uint32_t lane16) {
-  const uint32_t hdr = bcast(wv, 0);
+// Signed sum U = sum h x of the word block blk (uniform address; hdr = its
+// word 0), digit-wise: (U0, U1) for each polynomial.  The two 25-bit digits
+// of an input are added as one 64-bit word (the halves never carry into each
+// other for at most 48 members), in batches of kSumBatch LDS reads whose row
+// offsets come from scalar loads.
+__device__ __forceinline__ uint4 signed_sum(const uint32_t *blk, uint32_t hdr, const uint4 *lds, uint32_t lane16) {
+  const uint32_t np = hdr & 0xFFFFu, nn = hdr >> 16;
   uint64_t pa = 0, pb = 0, na = 0, nb = 0;
-  sum_rows<0>(hdr & 0xFFFFu, hdr >> 16, pa, pb, na, nb, wv, lds, lane16);
+#pragma unroll
+  for (uint32_t k = 0; k < kSumBatches; ++k) {
+    if (k * kSumBatch < np) sum_batch(pa, pb, sload4(blk + kAddWord + k * kSumBatch), lds, lane16);
+    if (k * kSumBatch < nn) sum_batch(na, nb, sload4(blk + kSumWords - (k + 1) * kSumBatch), lds, lane16);
+  }
   return make_uint4((uint32_t)pa - (uint32_t)na, (uint32_t)(pa >> 32) - (uint32_t)(na >> 32),
                     (uint32_t)pb - (uint32_t)nb, (uint32_t)(pb >> 32) - (uint32_t)(nb >> 32));
 }
-
-// Scalar (SMEM) loads of plan records.  Every wavefront of every tile reads
-// the same records, so they come from the scalar cache straight into SGPRs:
-// no vector load and no v_readlane per record.  The address must be uniform.
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
-typedef const __attribute__((address_space(4))) uint32_t *cu32p;
-typedef const __attribute__((address_space(4))) u32x2 *cu32x2p;
-typedef const __attribute__((address_space(4))) u32x4 *cu32x4p;
-typedef const __attribute__((address_space(4))) u32x16 *cu32x16p;
-__device__ __forceinline__ uint32_t sload1(const void *p) { return *(cu32p)p; }
-__device__ __forceinline__ u32x2 sload2(const void *p) { return *(cu32x2p)p; }
-__device__ __forceinline__ u32x4 sload4(const void *p) { return *(cu32x4p)p; }
-__device__ __forceinline__ u32x16 sload16(const void *p) { return *(cu32x16p)p; }
-__device__ __forceinline__ uint4 as_uint4(u32x4 v) { return make_uint4(v.x, v.y, v.z, v.w); }
-__device__ __forceinline__ uint2 as_uint2(u32x2 v) { return make_uint2(v.x, v.y); }
-
-typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
-typedef const __attribute__((address_space(4))) u32x8 *cu32x8p;
-__device__ __forceinline__ u32x8 sload8(const void *p) { return *(cu32x8p)p; }
 
 // Raw-term chunks.  A chunk block holds kChunkSlots plaintext offsets, then
 // kChunkSlots input rows; record r < 8 nb is (offset r, row r): the byte
@@ -271,9 +266,6 @@ __device__ __forceinline__ void fold(Acc &a0, Acc &a1, uint64_t &r0, uint64_t &r
   acc_zero(a1);
 }
 
-__device__ __forceinline__ uint4 load_use_chunk(const uint4 *uses, uint32_t begin, uint32_t count, uint32_t lane) {
-  return lane < count ? uses[begin + lane] : make_uint4(0, kInlineSum, 0, 0);
-}
 
 // Plan records of the main kernel (device pointers into the plan's image).
 struct KPlan {
@@ -285,9 +277,7 @@ struct KPlan {
   const uint32_t *flush;    // per buffered output: its output index (buffer row = entry - first)
   const uint4 *splits;      // per split output: output, first segment slot, segments
   const uint2 *pm;          // raw-term chunk blocks
-  const uint4 *uses;        // signed-sum uses
-  const uint32_t *mats;     // per resident sum: its word block
-  const uint32_t *words;    // word blocks of the common partial sums and distinct signed sums
+  const uint32_t *words;    // word blocks: common partial sums, resident signed sums, uses
 };
 
 template <int NW>
@@ -299,8 +289,6 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
   const uint4 *__restrict__ items = K.items;
   const uint32_t *__restrict__ dest = K.dest;
   const uint2 *__restrict__ pm = K.pm;
-  const uint4 *__restrict__ uses = K.uses;
-  const uint32_t *__restrict__ mats = K.mats;
   const uint32_t *__restrict__ words = K.words;
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t lane16 = lane * 16u;
@@ -330,7 +318,8 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
   for (uint32_t lv = 0, p0 = 0; lv < S.n_levels; ++lv) {
     const uint32_t p1 = S.level_end[lv];
     for (uint32_t p = p0 + wave; p < p1; p += NW) {
-      const uint4 U = signed_sum(words[(size_t)p * kSumWords + lane], lds, lane16);
+      const uint32_t *blk = words + (size_t)p * kSumWords;
+      const uint4 U = signed_sum(blk, sload1(blk), lds, lane16);
       const uint64_t v0 = reduce_i64((int64_t)(int32_t)U.x + ((int64_t)(int32_t)U.y << 25), lc.q, lc.qinv);
       const uint64_t v1 = reduce_i64((int64_t)(int32_t)U.z + ((int64_t)(int32_t)U.w << 25), lc.q, lc.qinv);
       parts[p * kTile + lane] = make_uint4(lo_digit(v0), hi_digit(v0), lo_digit(v1), hi_digit(v1));
@@ -342,8 +331,10 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
   // 3. shared signed sums, formed once per tile
   uint4 *sums = parts + (size_t)S.n_part * kTile;
   if (S.n_mat) {   // uniform over the workgroup
-    for (uint32_t s = wave; s < S.n_mat; s += NW)
-      sums[s * kTile + lane] = signed_sum(words[(size_t)mats[s] + lane], lds, lane16);
+    for (uint32_t s = wave; s < S.n_mat; s += NW) {
+      const uint32_t *blk = words + (size_t)(S.n_part + s) * kSumWords;
+      sums[s * kTile + lane] = signed_sum(blk, sload1(blk), lds, lane16);
+    }
     __syncthreads();
   }
 
@@ -356,22 +347,8 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
   const uint32_t out_row = limb * S.N + k0;   // offset of this tile in one output polynomial
   for (uint32_t rd = 0; rd < S.n_rounds; ++rd) {
   const uint2 wr = as_uint2(sload2(K.waves + rd * NW + wave));
-  uint4 item_next = wr.y ? as_uint4(sload4(items + wr.x)) : make_uint4(0, 0, 0, 0);
-  uint4 use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
   for (uint32_t it = wr.x; it < wr.x + wr.y; ++it) {
-    const uint4 item = item_next;   // first chunk, chunks, first use, uses
-    uint4 use_rec = use_next;
-    if (it + 1 < wr.x + wr.y) {
-      item_next = as_uint4(sload4(items + it + 1));
-      use_next = load_use_chunk(uses, item_next.z, min(64u, item_next.w), lane);
-    }
-    // word blocks of this item's first two uses (loaded before the raw route,
-    // so waiting for them never waits for plaintext loads)
-    uint32_t wq0 = 0, wq1 = 0;
-    if (item.w) {
-      wq0 = words[(size_t)bcast(use_rec.x, 0) + lane];
-      wq1 = words[(size_t)(item.w > 1 ? bcast(use_rec.x, 1) : 0u) + lane];
-    }
+    const uint4 item = as_uint4(sload4(items + it));   // first chunk, chunks, first use, uses
     Acc a0, a1;
     acc_zero(a0);
     acc_zero(a1);
@@ -387,37 +364,17 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
       raw_chunk(sload_block(pm, item.x + c), pt_tile, voff, a0, a1, lds, lane16);
     }
 
-    // signed route: each use applies its group's scale once to a signed sum.
-    // Word blocks are loaded two uses ahead, on every path (a resident sum's,
-    // or block 0 past the end, is loaded and not used), so each use waits
-    // only for its own block.
-    for (uint32_t base = 0; base < item.w; base += 64) {
-      const uint32_t n = min(64u, item.w - base);
-      // word begin, LDS slot or kInlineSum, scale index | negate << 31, signed scale
-      const uint4 rec = use_rec;
-      const bool more = base + 64 < item.w;
-      if (more) use_rec = load_use_chunk(uses, item.z + base + 64, min(64u, item.w - base - 64), lane);
-      if (base && base % kFoldUses == 0) fold(a0, a1, r0, r1, lc);
-      // word block of use base + j (j < n + 2), or block 0 past the item's end
-      auto block_of = [&](uint32_t j) -> size_t {
-        if (j < n) return bcast(rec.x, j);
-        return more ? bcast(use_rec.x, j - n) : 0u;
-      };
-      auto apply = [&](uint32_t r, uint32_t wq) {
-        const uint32_t slot = bcast(rec.y, r);
-        const uint4 U = slot != kInlineSum ? sums[slot * kTile + lane] : signed_sum(wq, lds, lane16);
-        const int32_t c = (int32_t)bcast(rec.w, r);
-        smac(a0, c, (int32_t)U.x, (int32_t)U.y);
-        smac(a1, c, (int32_t)U.z, (int32_t)U.w);
-      };
-      uint32_t r = 0;
-      for (; r + 1 < n; r += 2) {
-        apply(r, wq0);
-        wq0 = words[block_of(r + 2) + lane];
-        apply(r + 1, wq1);
-        wq1 = words[block_of(r + 3) + lane];
-      }
-      if (r < n) apply(r, wq0);   // an odd count: only the item's last use chunk
+    // signed route: each use applies its group's scale once to a signed sum,
+    // read from LDS (a resident sum) or formed in place from the use's block
+    const uint32_t *ub = words + (size_t)(S.use_block0 + item.z) * kSumWords;
+    for (uint32_t u = 0; u < item.w; ++u) {
+      if (u && u % kFoldUses == 0) fold(a0, a1, r0, r1, lc);
+      const uint32_t *blk = ub + (size_t)u * kSumWords;
+      const u32x4 hd = sload4(blk);   // row counts, resident slot or kInlineSum, signed scale
+      const uint4 U = hd.y != kInlineSum ? sums[hd.y * kTile + lane] : signed_sum(blk, hd.x, lds, lane16);
+      const int32_t c = (int32_t)hd.z;
+      smac(a0, c, (int32_t)U.x, (int32_t)U.y);
+      smac(a1, c, (int32_t)U.z, (int32_t)U.w);
     }
 
     const uint64_t y0 = finish(a0, r0, lc);
