@@ -325,6 +325,33 @@ def test_full_size_sampled(dev, name):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("name,width", [("vgg11", 2048), ("bert_ffn", 1024)])
+def test_full_size_contiguous_tiles(dev, name, width):
+    """Full-size layer in the benchmark's launch configuration: every output at
+    every coefficient of a run of whole tiles at the start of limb 0 and at the
+    end of the last limb (32 resp. 16 tiles each), element by element."""
+    import torch
+    layer = synth.make_layer(synth.CONFIGS[name], 1)
+    out_t, in_t, pt_t, plan = _run(layer, dev, pitch="hint")
+    _say("[parity] %s full size, %d contiguous coefficients in the first and last limb" % (name, width))
+    del pt_t
+    L, N = layer.L, layer.N
+    limbs = np.concatenate([np.zeros(width, np.int64), np.full(width, L - 1, np.int64)])
+    coeffs = np.concatenate([np.arange(width), np.arange(N - width, N)]).astype(np.int64)
+    x_s = synth.input_values(layer, (limbs, coeffs))
+    pt_s = synth.pt_values(layer, (limbs, coeffs))
+    expect = oracle.weighted_sum_sampled(layer, limbs, coeffs, x_s, pt_s, n_threads=16)
+    del pt_s
+    got = out_t[: layer.n_out * 2 * L * N].view(layer.n_out, 2, L, N)[:, :, limbs, coeffs].cpu().numpy().view(np.uint64)
+    bad = np.argwhere(got != expect)
+    if bad.size:
+        j, p, i = (int(v) for v in bad[0])
+        raise AssertionError("%s: %d mismatches; first at out %d poly %d limb %d coeff %d"
+                             % (name, len(bad), j, p, limbs[i], coeffs[i]))
+    del out_t, in_t
+    torch.cuda.empty_cache()
+
+
 def test_full_size_large_all_chunks(dev):
     import torch
     import synth.gpu
