@@ -129,6 +129,64 @@ def time_layer(layer, dev, steps, warmup, stream, label, flags=0, padded=True):
     return total_ms, total_bytes, per_chunk
 
 
+def time_plan_variants(layer, dev, steps, warmup, stream, variants, padded=True, rounds=3):
+    """Time plans compiled under different flags on the SAME device buffers (one
+    allocation per buffer, every chunk's plaintexts filled once), interleaving
+    the variants over `rounds` rounds and keeping each one's best round: the
+    physical placement of a fresh allocation moves a layer's time by several
+    percent, which would otherwise swamp the differences between plans.
+    variants: [(name, flags)]; returns {name: (sum of per-chunk ms, summed plan counts)}."""
+    import torch
+    import synth
+    import synth.gpu
+    import paper_2609_35352_amd as fiona
+
+    cfg = layer.cfg
+    chunks = synth.output_chunks(layer.n_out, cfg.chunks_hybrid if layer.pt_const is None else cfg.chunks_allpm)
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    pitch = ctx.pt_pitch_hint() if padded is True else (layer.L * layer.N if padded is False
+                                                        else layer.L * layer.N + int(padded))
+    subs = [synth.chunk_layer(layer, a, b) for a, b in chunks]
+    in_t = torch.empty(layer.n_in * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_inputs(layer, in_t)
+    max_pt = max(max(1, s.n_pt) for s in subs)
+    pt_t = torch.empty((max_pt - 1) * pitch + layer.L * layer.N, dtype=torch.int64, device=dev)
+    out_t = torch.empty(max(s.n_out for s in subs) * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    res = {name: [0.0, {}] for name, _ in variants}
+    for ci, sub in enumerate(subs):
+        synth.gpu.fill_pts(sub, pt_t, pitch)
+        sign_t = torch.from_numpy(np.ascontiguousarray(sub.mem_sign)).to(dev) if sub.mem_sign.size else \
+            torch.zeros(1, dtype=torch.int8, device=dev)
+        scale_t = torch.from_numpy(np.ascontiguousarray(sub.scales.view(np.int64))).to(dev) if sub.scales.size \
+            else torch.zeros(1, dtype=torch.int64, device=dev)
+        plans = {name: fiona.Plan.from_layer(ctx, sub, flags=flags, pt_pitch=pitch) for name, flags in variants}
+        best = {name: float("inf") for name, _ in variants}
+        torch.cuda.synchronize()
+        for rd in range(rounds):
+            for name, _ in variants:
+                for _ in range(warmup if rd == 0 else 1):
+                    fiona.hybrid_linear(plans[name], in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(steps):
+                    fiona.hybrid_linear(plans[name], in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                best[name] = min(best[name], e0.elapsed_time(e1) / steps)
+        for name, _ in variants:
+            res[name][0] += best[name]
+            st = plans[name].stats()
+            for key in ("pmult_grouped", "n_use", "addsub_partial", "n_partial", "n_sum_distinct"):
+                res[name][1][key] = res[name][1].get(key, 0) + st[key]
+        log("[bench] plan variants, chunk %d/%d: %s" % (ci + 1, len(subs),
+                                                        ", ".join("%s %.3f ms" % (n, best[n]) for n, _ in variants)))
+        del plans
+    del pt_t, out_t, in_t
+    torch.cuda.empty_cache()
+    return {name: (ms, counts) for name, (ms, counts) in res.items()}
+
+
 def time_rescale(layer, dev, steps, warmup, stream):
     """Time fiona_rescale on n_out ciphertexts of the layer's shape (device-generated
     residues), all outputs in one call."""
@@ -272,14 +330,15 @@ def main():
         # the compilations of Sec. 6.2 on the same kernel: every signed term's
         # factor applied on its own, then grouping, then sharing whole sums,
         # then sharing partly overlapping sums as well (the default plan)
+        # (all four on the same buffers, interleaved: see time_plan_variants)
         ablation = []
-        for name, flags in (("per-contribution", fiona.FIONA_PLAN_PER_CONTRIBUTION),
-                            ("+grouping", fiona.FIONA_PLAN_NO_SHARING),
-                            ("+sharing", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
-                            ("+partial sharing", 0)):
-            ms, _, _ = time_layer(layer, dev, args.steps, args.warmup, stream, name, flags,
-                                  padded=pad_mode)
-            c = time_layer.counts
+        variants = (("per-contribution", fiona.FIONA_PLAN_PER_CONTRIBUTION),
+                    ("+grouping", fiona.FIONA_PLAN_NO_SHARING),
+                    ("+sharing", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
+                    ("+partial sharing", 0))
+        timed = time_plan_variants(layer, dev, args.steps, args.warmup, stream, variants, padded=pad_mode)
+        for name, _ in variants:
+            ms, c = timed[name]
             ablation.append({"plan": name, "ms_per_step": round(ms, 4),
                              "value": round(layer.ct_terms / (ms * 1e-3), 1),
                              "scalar_products": c["n_use"], "pmult": c["pmult_grouped"] - c["n_use"],
