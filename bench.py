@@ -35,11 +35,39 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def strip_comments(src: str) -> str:
+    """C++ source without its comments, whitespace runs collapsed (string and
+    character literals kept as they are)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
+    """Hash of the hybrid kernel's code (comments excluded), which the committed
+    counter records name: a change of code makes them stale, a change of
+    comments does not."""
     h = hashlib.sha256()
     for name in ("fiona.hip", "hybrid_kernel.hpp", "modarith.hpp"):
-        with open(os.path.join(ROOT, "paper_2609_35352_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2609_35352_amd", "csrc", name), encoding="utf-8") as f:
+            h.update(strip_comments(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -20,11 +20,10 @@
 //      and Raw Routes"), reduced once to a canonical residue.  A whole output
 //      is written at once; the segments of a split output leave their
 //      residues in LDS and are added after a barrier.
-// Plan records are wave-uniform.  Work items and raw-term records are read
-// with scalar loads straight into SGPRs (every tile reads the same records, so
-// they stay in the scalar cache); the use records and member words of signed
-// sums are loaded one per lane with a vector load and broadcast with
-// v_readlane.  All control flow is uniform.  No MFMA: this is modular integer
+// Plan records are wave-uniform.  Work items, raw-term records, use headers
+// and the member words of signed sums are all read with scalar loads straight
+// into SGPRs (every tile reads the same records, so they stay in the scalar
+// cache).  All control flow is uniform.  No MFMA: this is modular integer
 // arithmetic.
 #pragma once
 #include <hip/hip_runtime.h>
