@@ -55,6 +55,8 @@ def lib():
         for name in ("oracle_ntt_fast", "oracle_intt_fast"):
             getattr(L, name).restype = ctypes.c_int
             getattr(L, name).argtypes = [_u64p, _u64p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64]
+        L.oracle_mul_acc.restype = None
+        L.oracle_mul_acc.argtypes = [_u64p, _u64p, _u64p, ctypes.c_uint32, ctypes.c_uint64]
         L.oracle_negacyclic_mul.restype = None
         L.oracle_negacyclic_mul.argtypes = [_u64p, _u64p, _u64p, ctypes.c_uint32, ctypes.c_uint64]
         _lib = L
@@ -167,3 +169,11 @@ def negacyclic_mul(a, b, q):
     c = np.zeros(len(a), dtype=np.uint64)
     lib().oracle_negacyclic_mul(_p(a, _u64p), _p(b, _u64p), _p(c, _u64p), len(a), q)
     return c
+
+
+def mul_acc(acc, a, b, q):
+    """acc + a * b (mod q), element-wise; acc is updated in place and returned."""
+    a, b = _c(a, np.uint64), _c(b, np.uint64)
+    assert acc.dtype == np.uint64 and acc.flags.c_contiguous and len(acc) == len(a) == len(b)
+    lib().oracle_mul_acc(_p(acc, _u64p), _p(a, _u64p), _p(b, _u64p), len(a), q)
+    return acc

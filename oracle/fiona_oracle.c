@@ -265,3 +265,9 @@ void oracle_negacyclic_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, ui
     }
   }
 }
+
+/* acc_k = (acc_k + a_k b_k) mod q for k < N: one term of an element-wise
+ * (NTT-domain) inner product, used by the rotation oracle's key switching. */
+void oracle_mul_acc(uint64_t *acc, const uint64_t *a, const uint64_t *b, uint32_t N, uint64_t q) {
+  for (uint32_t k = 0; k < N; ++k) acc[k] = addmod(acc[k], mulmod(a[k] % q, b[k] % q, q), q);
+}
