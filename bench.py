@@ -215,6 +215,52 @@ def time_plan_variants(layer, dev, steps, warmup, stream, variants, padded=True,
     return {name: (ms, counts) for name, (ms, counts) in res.items()}
 
 
+def time_rotate(layer, dev, steps, warmup, stream):
+    """Time fiona_hoisted_rotate: the layer's n_in - 1 baby-step rotations
+    (by 1 .. n_in - 1 slots) of one ciphertext, one call, device-generated
+    ciphertext and keys (uniform residues, already in the library's layout)."""
+    import torch
+    import synth
+    import synth.gpu
+    import paper_2609_35352_amd as fiona
+
+    N, L = layer.N, layer.L
+    primes = synth.ntt_primes(N, L + 1)
+    if [int(q) for q in layer.moduli] != primes[:L]:
+        raise ValueError("the layer's moduli are not the first L primes of the modulus rule")
+    P = primes[L]
+    steps_r = list(range(1, layer.n_in))
+    galois = [pow(5, r, 2 * N) for r in steps_r]
+    n = len(galois)
+    ctx = fiona.Ctx(N, L, layer.moduli)
+    rot = fiona.Rotator(ctx, P, n)
+    kw = rot.key_words()
+    ct_t = torch.empty(2 * L * N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_cts(layer, ct_t, 1)
+    keys_t = torch.empty(n * kw, dtype=torch.int64, device=dev)
+    synth.gpu.fill_rows(keys_t, n * kw // N, list(layer.moduli) + [P], N, layer.seed, synth.TAG_KEY)
+    out_t = torch.empty(n * 2 * L * N, dtype=torch.int64, device=dev)
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        fiona.hoisted_rotate(rot, ct_t, galois, keys_t, out_t, stream=stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        fiona.hoisted_rotate(rot, ct_t, galois, keys_t, out_t, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    nbytes = 8 * (2 * L * N + n * kw + n * 2 * L * N)
+    log("[bench] %d hoisted rotations (N=%d, L=%d): %.3f ms, %.1f GB/s algorithmic"
+        % (n, N, L, ms, nbytes / ms / 1e6))
+    del keys_t, out_t, ct_t, rot
+    torch.cuda.empty_cache()
+    return {"rotations": n, "special_prime": P, "ms": round(ms, 4), "rotations_per_s": round(n / (ms * 1e-3), 1),
+            "alg_bytes": nbytes, "alg_GBps": round(nbytes / ms / 1e6, 1),
+            "frac_of_hbm_peak": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4)}
+
+
 def time_rescale(layer, dev, steps, warmup, stream):
     """Time fiona_rescale on n_out ciphertexts of the layer's shape (device-generated
     residues), all outputs in one call."""
@@ -284,6 +330,9 @@ def main():
     ap.add_argument("--no-allpmult", action="store_true", help="time only the hybrid layer")
     ap.add_argument("--only-allpmult", action="store_true", help="time only the all-PMult layer")
     ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--rotate", action="store_true",
+                    help="also time the hoisted baby-step rotations that produce the layer's inputs "
+                         "(fiona_hoisted_rotate)")
     ap.add_argument("--rescale", action="store_true",
                     help="also time the rescale epilogue on the layer's outputs (fiona_rescale)")
     ap.add_argument("--ablation", action="store_true",
@@ -377,6 +426,9 @@ def main():
     rescale = None
     if args.rescale:
         rescale = time_rescale(layer, dev, args.steps, args.warmup, stream)
+    rotate = None
+    if args.rotate:
+        rotate = time_rotate(layer, dev, args.steps, args.warmup, stream)
     wall = time.perf_counter() - t_wall0
 
     traffic = measured_traffic(cfg.name, "hybrid")
@@ -409,6 +461,7 @@ def main():
         "hybrid_chunks": hy_chunks if n_launch > 1 else None,
         "ablation": ablation,
         "rescale": rescale,
+        "rotate": rotate,
         "gpu_wall_s": round(wall, 2),
     }
     if not args.no_cpu_baseline:

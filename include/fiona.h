@@ -267,6 +267,70 @@ void fiona_rescaler_destroy(fiona_rescaler *rescaler);
 int fiona_rescale(const fiona_rescaler *rescaler, const uint64_t *in_cts, uint32_t n_ct, uint64_t *out_cts,
                   hipStream_t stream);
 
+/*
+ * Hoisted baby-step rotations: the step that produces fiona_hybrid_linear's
+ * input ciphertexts.  A layer's inputs A_i are the packed input rotated by
+ * the packing layout's baby steps (paper Sec. 2 "Homomorphic Operations": Rot
+ * cyclically shifts the slots; Sec. 4.2: the A_i are prepared according to
+ * the packing layout).  Rot by r slots is the automorphism sigma_g:
+ * a(X) -> a(X^g), g = 5^r mod 2N (slot j of a message is its value at
+ * zeta^(5^j), zeta = exp(i pi / N)), on both polynomials, followed by a key
+ * switch of the second polynomial from sigma_g(s) back to s.  Key switching
+ * decomposes c1 by RNS limb (digit j = the coefficients of c1 mod q_j, as
+ * integers in [0, q_j)), multiplies digit j by key polynomial pair j over the
+ * data moduli and one special prime P, sums, and divides by P with rounding:
+ *     Rot(c0, c1) = (sigma(c0) + v_0, v_1),
+ *     v_p = round(sum_j sigma(D_j) ksk[j][p] / P)    (coefficient-wise).
+ * The digits are formed once per call and shared by all its rotations
+ * (hoisting); the automorphism acts on the integer digits.  NTT convention:
+ * as for the rescaler, for every modulus including P.
+ *
+ * fiona_rotator_create: NTT tables of q_0 .. q_{L-1} and P, and a workspace
+ * for up to max_rot rotations per call (about 8 N (L (L+1) 2 + max_rot (4 L + 6))
+ * bytes).
+ *   special_prime  P with 2^20 < P < 2^50, P = 1 mod 2N, unequal to every q_l
+ *   psi            host [L + 1] roots (the data moduli, then P) or NULL for
+ *                  the defaults of fiona_rescaler_create
+ * Requires N a power of two in [2^8, 2^17] and L + 1 <= FIONA_MAX_L.  Keeps a
+ * reference to ctx.  Errors: FIONA_ERR_ARG, FIONA_ERR_UNSUPPORTED,
+ * FIONA_ERR_NOMEM, FIONA_ERR_HIP.
+ *
+ * Keys.  A rotation's key holds, for digit j < L and polynomial p in {0, 1},
+ * one polynomial over the L + 1 moduli, NTT domain: [L][2][L + 1][N] uint64
+ * canonical residues, modulus index L being P (fiona_rotation_key_words
+ * words).  In its natural order, sum_j D_j ksk[j][0] + (sum_j D_j ksk[j][1]) s
+ * = P D sigma_g(s) + small for a key that switches sigma_g(s) to s.
+ * fiona_hoisted_rotate reads keys in the library's layout: each row of N
+ * words permuted by the rotation's slot map, written by
+ * fiona_rotation_key_layout from a key in natural order (once per key).
+ *
+ * fiona_rotation_key_layout: key_out = the library layout of key (both device,
+ *   fiona_rotation_key_words words, not overlapping) for Galois element
+ *   galois (odd, < 2N).  Asynchronous on stream; allocates nothing.
+ *
+ * fiona_hoisted_rotate: n_rot rotations of one ciphertext.
+ *   ct       device, [2][L][N] canonical residues (NTT domain)
+ *   galois   host, [n_rot] Galois elements (odd, < 2N; 5^r mod 2N rotates by r)
+ *   keys     device, [n_rot] keys in the library layout, key r for galois[r]
+ *   out_cts  device, [n_rot][2][L][N], overwritten with canonical residues;
+ *            must not overlap ct or keys
+ *   n_rot    at most the rotator's max_rot
+ * Asynchronous on stream; allocates nothing.  The workspace is shared by the
+ * rotator's calls: one rotator must not be used by two streams at the same
+ * time.  Results are exact: bit-identical to the definition above computed
+ * in integers.  Errors (nothing is launched): FIONA_ERR_ARG, FIONA_ERR_ALIGN,
+ * FIONA_ERR_ALIAS, FIONA_ERR_HIP.
+ */
+typedef struct fiona_rotator fiona_rotator;
+int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uint64_t *psi, uint32_t max_rot,
+                         fiona_rotator **out);
+void fiona_rotator_destroy(fiona_rotator *rotator);
+uint64_t fiona_rotation_key_words(const fiona_rotator *rotator);
+int fiona_rotation_key_layout(const fiona_rotator *rotator, uint32_t galois, const uint64_t *key,
+                              uint64_t *key_out, hipStream_t stream);
+int fiona_hoisted_rotate(const fiona_rotator *rotator, const uint64_t *ct, uint32_t n_rot, const uint32_t *galois,
+                         const uint64_t *keys, uint64_t *out_cts, hipStream_t stream);
+
 /* Static string naming a status code. */
 const char *fiona_status_string(int status);
 

@@ -267,3 +267,83 @@ def rescale(rescaler: Rescaler, in_t, n_ct: int, out_t, stream=None) -> None:
     s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
     _check(lib().fiona_rescale(rescaler.handle, _dptr(in_t, "in_cts", 8), int(n_ct), _dptr(out_t, "out_cts", 8), s),
            "fiona_rescale")
+
+
+class Rotator:
+    """NTT tables of the data moduli and the special prime, and the workspace of
+    the hoisted rotations (fiona_rotator_create)."""
+
+    def __init__(self, ctx: Ctx, special_prime: int, max_rot: int, psi=None):
+        L = lib()
+        L.fiona_rotator_create.restype = ctypes.c_int
+        L.fiona_rotator_create.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_uint32,
+                                           ctypes.POINTER(ctypes.c_void_p)]
+        L.fiona_rotator_destroy.restype = None
+        L.fiona_rotator_destroy.argtypes = [ctypes.c_void_p]
+        L.fiona_rotation_key_words.restype = ctypes.c_uint64
+        L.fiona_rotation_key_words.argtypes = [ctypes.c_void_p]
+        L.fiona_rotation_key_layout.restype = ctypes.c_int
+        L.fiona_rotation_key_layout.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
+                                                ctypes.c_void_p]
+        L.fiona_hoisted_rotate.restype = ctypes.c_int
+        L.fiona_hoisted_rotate.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        self.ctx = ctx
+        self.P = int(special_prime)
+        self.max_rot = int(max_rot)
+        roots = None
+        if psi is not None:
+            roots = (ctypes.c_uint64 * (ctx.L + 1))(*[int(p) for p in psi])
+        h = ctypes.c_void_p()
+        _check(L.fiona_rotator_create(ctx.handle, self.P, ctypes.cast(roots, ctypes.c_void_p) if roots else None,
+                                      self.max_rot, ctypes.byref(h)), "fiona_rotator_create")
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def key_words(self) -> int:
+        """Words of one rotation key: L * 2 * (L + 1) * N."""
+        return int(lib().fiona_rotation_key_words(self._h))
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib().fiona_rotator_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _stream_handle(stream):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def rotation_key_layout(rotator: Rotator, galois: int, key_t, out_t, stream=None) -> None:
+    """fiona_rotation_key_layout: a key [L][2][L+1][N] in natural NTT order -> the library's layout."""
+    n = rotator.key_words()
+    if key_t.numel() < n or out_t.numel() < n:
+        raise ValueError("key tensors need %d words" % n)
+    _check(lib().fiona_rotation_key_layout(rotator.handle, int(galois), _dptr(key_t, "key", 8),
+                                           _dptr(out_t, "key_out", 8), _stream_handle(stream)),
+           "fiona_rotation_key_layout")
+
+
+def hoisted_rotate(rotator: Rotator, ct_t, galois, keys_t, out_t, stream=None) -> None:
+    """fiona_hoisted_rotate: ct [2][L][N] -> out [len(galois)][2][L][N], keys [len(galois)] in the library layout."""
+    N, L = rotator.ctx.N, rotator.ctx.L
+    n_rot = len(galois)
+    if ct_t.numel() < 2 * L * N or out_t.numel() < n_rot * 2 * L * N or keys_t.numel() < n_rot * rotator.key_words():
+        raise ValueError("tensors too small for %d rotations" % n_rot)
+    g = (ctypes.c_uint32 * max(1, n_rot))(*[int(x) for x in galois])
+    _check(lib().fiona_hoisted_rotate(rotator.handle, _dptr(ct_t, "ct", 8), n_rot, ctypes.cast(g, ctypes.c_void_p),
+                                      _dptr(keys_t, "keys", 8), _dptr(out_t, "out_cts", 8), _stream_handle(stream)),
+           "fiona_hoisted_rotate")

@@ -1,0 +1,166 @@
+// Host side of the NTT passes (ntt_kernel.hpp): twiddle tables, the table
+// image in device memory, and the launch of one pass.  Shared by the rescale
+// epilogue (rescale.hip) and the rotation producer (rotate.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+#include "ntt_kernel.hpp"
+
+namespace fiona_host {
+
+using fiona::NttPass;
+using fiona::NttSet;
+using fiona::Tw;
+
+inline uint64_t mulmod_h(uint64_t a, uint64_t b, uint64_t q) { return (uint64_t)((unsigned __int128)a * b % q); }
+
+inline uint64_t powmod_h(uint64_t b, uint64_t e, uint64_t q) {
+  uint64_t r = 1 % q;
+  b %= q;
+  while (e) {
+    if (e & 1) r = mulmod_h(r, b, q);
+    b = mulmod_h(b, b, q);
+    e >>= 1;
+  }
+  return r;
+}
+
+inline Tw make_tw(uint64_t w, uint64_t q) { return Tw{(double)w, (double)w / (double)q}; }
+
+// The default root: psi = x^((q-1)/2N) for the smallest x >= 2 with psi^N = -1.
+inline uint64_t default_psi(uint32_t N, uint64_t q) {
+  for (uint64_t x = 2; x < 1000000; ++x) {
+    const uint64_t psi = powmod_h(x, (q - 1) / (2ull * N), q);
+    if (powmod_h(psi, N, q) == q - 1) return psi;
+  }
+  return 0;
+}
+
+// Tables of one direction of one modulus.  Forward: pre = psi^n, mid =
+// omega^(n1 k2) at k2 N1 + n1, DFT roots omega^N1 (size N2) and omega^N2
+// (size N1).  Inverse: omega -> omega^-1, no pre, post = N^-1 psi^-k.
+struct TableSet {
+  std::vector<Tw> pre, mid, dft_a, dft_b, post;
+};
+
+inline TableSet make_tables(uint32_t log_n1, uint32_t log_n2, uint64_t q, uint64_t psi, bool inverse) {
+  const uint32_t N1 = 1u << log_n1, N2 = 1u << log_n2, N = N1 * N2;
+  const uint64_t psi_inv = powmod_h(psi, q - 2, q);
+  const uint64_t omega = inverse ? mulmod_h(psi_inv, psi_inv, q) : mulmod_h(psi, psi, q);
+  TableSet t;
+  if (!inverse) {
+    t.pre.resize(N);
+    uint64_t p = 1;
+    for (uint32_t n = 0; n < N; ++n, p = mulmod_h(p, psi, q)) t.pre[n] = make_tw(p, q);
+  } else {
+    t.post.resize(N);
+    uint64_t p = powmod_h(N, q - 2, q);
+    for (uint32_t n = 0; n < N; ++n, p = mulmod_h(p, psi_inv, q)) t.post[n] = make_tw(p, q);
+  }
+  t.mid.resize(N);
+  for (uint32_t n1 = 0; n1 < N1; ++n1) {
+    const uint64_t step = powmod_h(omega, n1, q);
+    uint64_t p = 1;
+    for (uint32_t k2 = 0; k2 < N2; ++k2, p = mulmod_h(p, step, q)) t.mid[(size_t)k2 * N1 + n1] = make_tw(p, q);
+  }
+  const uint64_t w2 = powmod_h(omega, N1, q), w1 = powmod_h(omega, N2, q);
+  t.dft_a.resize(N2 / 2);
+  uint64_t p = 1;
+  for (uint32_t i = 0; i < N2 / 2; ++i, p = mulmod_h(p, w2, q)) t.dft_a[i] = make_tw(p, q);
+  t.dft_b.resize(N1 / 2);
+  p = 1;
+  for (uint32_t i = 0; i < N1 / 2; ++i, p = mulmod_h(p, w1, q)) t.dft_b[i] = make_tw(p, q);
+  return t;
+}
+
+// Host image of table sets: all tables back to back (Tw), then the NttSet
+// records, which point into the device copy of the same image.
+struct TableImage {
+  std::vector<Tw> tw;
+  struct Entry {
+    size_t pre, mid, dft_a, dft_b, post;
+    uint64_t q;
+    Tw inv;
+  };
+  std::vector<Entry> entries;
+
+  // Appends the tables of one modulus; returns its set index.
+  uint32_t add(const TableSet &t, uint64_t q, Tw inv = Tw{0.0, 0.0}) {
+    auto put = [&](const std::vector<Tw> &v) {
+      const size_t o = tw.size();
+      tw.insert(tw.end(), v.begin(), v.end());
+      return v.empty() ? (size_t)-1 : o;
+    };
+    Entry e{put(t.pre), put(t.mid), put(t.dft_a), put(t.dft_b), put(t.post), q, inv};
+    entries.push_back(e);
+    return (uint32_t)entries.size() - 1;
+  }
+
+  size_t table_bytes() const { return (tw.size() * sizeof(Tw) + 255) / 256 * 256; }
+  size_t bytes() const { return table_bytes() + (entries.size() * sizeof(NttSet) + 255) / 256 * 256; }
+
+  // Copies the image to dev (bytes() long); returns the device NttSet array.
+  NttSet *upload(void *dev) const {
+    const Tw *tb = (const Tw *)dev;
+    auto at = [&](size_t o) { return o == (size_t)-1 ? nullptr : tb + o; };
+    std::vector<NttSet> sets;
+    for (const Entry &e : entries)
+      sets.push_back(NttSet{at(e.pre), at(e.mid), at(e.dft_a), at(e.dft_b), at(e.post), e.inv, (double)e.q,
+                            1.0 / (double)e.q});
+    NttSet *dsets = (NttSet *)((char *)dev + table_bytes());
+    if (hipMemcpy(dev, tw.data(), tw.size() * sizeof(Tw), hipMemcpyHostToDevice) != hipSuccess) return nullptr;
+    if (hipMemcpy(dsets, sets.data(), sets.size() * sizeof(NttSet), hipMemcpyHostToDevice) != hipSuccess)
+      return nullptr;
+    return dsets;
+  }
+};
+
+// The passes are instantiated per DFT side 2^4 .. 2^9.
+template <uint32_t LOG>
+void launch_pair(bool a, dim3 grid, size_t smem, hipStream_t stream, const NttPass &P) {
+  if (a) hipLaunchKernelGGL(fiona::ntt_pass_a<LOG>, grid, dim3(fiona::kNttThreads), smem, stream, P);
+  else hipLaunchKernelGGL(fiona::ntt_pass_b<LOG>, grid, dim3(fiona::kNttThreads), smem, stream, P);
+}
+
+// One pass over gridDim.y = V vectors (V <= 65535).
+inline void launch_pass(bool a, uint32_t log_side, uint32_t log_other, uint32_t V, hipStream_t stream,
+                        const NttPass &P) {
+  const dim3 grid((1u << log_other) / fiona::kNttCols, V);
+  const size_t smem = fiona::kNttCols * fiona::padded_len(1u << log_side) * sizeof(double) +
+                      (1u << log_side) / 2 * sizeof(Tw);
+  switch (log_side) {
+    case 4: launch_pair<4>(a, grid, smem, stream, P); break;
+    case 5: launch_pair<5>(a, grid, smem, stream, P); break;
+    case 6: launch_pair<6>(a, grid, smem, stream, P); break;
+    case 7: launch_pair<7>(a, grid, smem, stream, P); break;
+    case 8: launch_pair<8>(a, grid, smem, stream, P); break;
+    default: launch_pair<9>(a, grid, smem, stream, P); break;
+  }
+}
+
+// Both passes of one transform.
+inline void launch_transform(uint32_t log_n1, uint32_t log_n2, uint32_t V, hipStream_t stream, const NttPass &P) {
+  launch_pass(true, log_n2, log_n1, V, stream, P);
+  launch_pass(false, log_n1, log_n2, V, stream, P);
+}
+
+template <uint32_t LOG>
+bool allow_smem_one(int bytes) {
+  return hipFuncSetAttribute((const void *)fiona::ntt_pass_a<LOG>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             bytes) == hipSuccess &&
+         hipFuncSetAttribute((const void *)fiona::ntt_pass_b<LOG>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             bytes) == hipSuccess;
+}
+
+// Lets every pass use the LDS of its largest side.
+inline bool allow_smem() {
+  const int smem = (int)(fiona::kNttCols * fiona::padded_len(fiona::kNttMaxSide) * sizeof(double) +
+                         fiona::kNttMaxSide / 2 * sizeof(Tw));
+  return allow_smem_one<4>(smem) && allow_smem_one<5>(smem) && allow_smem_one<6>(smem) &&
+         allow_smem_one<7>(smem) && allow_smem_one<8>(smem) && allow_smem_one<9>(smem);
+}
+
+}  // namespace fiona_host

@@ -165,25 +165,37 @@ enum NttStore : uint32_t {
   kStoreRescale = 2,  // (base - transform) * inv mod q, in [0, q) as uint64
 };
 
+// One modulus of a pass and its tables.
+struct NttSet {
+  const Tw *pre;     // pass A: multiply input n by pre[n] (null: by 1)
+  const Tw *mid;     // pass A: mid[k2 N1 + n1] = omega^(n1 k2)
+  const Tw *dft_a;   // size-N2 DFT twiddles (N2 / 2)
+  const Tw *dft_b;   // size-N1 DFT twiddles (N1 / 2)
+  const Tw *post;    // pass B: multiply output k by post[k] (null: by 1)
+  Tw inv;            // kStoreRescale: the factor applied after the subtraction
+  double q, qinv;    // the modulus and fl(1 / q)
+};
+
+// A launch covers vectors v = 0 .. gridDim.y - 1, grouped into sets of vps
+// consecutive vectors that share one modulus: vector v is number v % vps of
+// set v / vps, whose modulus and tables are sets[v / vps].  Its words sit at
+//   in   + (v / vps) * in_set_stride   + (v % vps) * in_stride   + n,
+// and likewise for out and base; the intermediate of vector v at tmp + v * N.
 struct NttPass {
-  const void *in;        // pass A: vector v, element n at in + v * in_stride + n
-  double *tmp;           // the transposed intermediate, vector v at tmp + v * N
-  void *out;             // pass B: vector v, element k at out + v * out_stride + k
-  const uint64_t *base;  // kStoreRescale: base + v * base_stride + k, residues in [0, q)
-  const Tw *pre;         // pass A: multiply input n by pre[n] (null: by 1)
-  const Tw *mid;         // pass A: mid[k2 N1 + n1] = omega^(n1 k2)
-  const Tw *dft_a;       // size-N2 DFT twiddles (N2 / 2)
-  const Tw *dft_b;       // size-N1 DFT twiddles (N1 / 2)
-  const Tw *post;        // pass B: multiply output k by post[k] (null: by 1)
-  Tw inv;                // kStoreRescale: the factor applied after the subtraction
-  double q, qinv;        // the modulus and fl(1 / q)
+  const void *in;        // pass A input
+  double *tmp;           // the transposed intermediates
+  void *out;             // pass B output
+  const uint64_t *base;  // kStoreRescale: residues in [0, q)
+  const NttSet *sets;    // device array, one entry per set
   uint64_t in_stride, out_stride, base_stride;
-  uint32_t log_n1, log_n2, load, store;
+  uint64_t in_set_stride, out_set_stride, base_set_stride;
+  uint32_t vps, log_n1, log_n2, load, store;
 };
 
 // Global loads and stores go in batches of up to kNttBatch per thread, all
-// issued before the first is used.
-constexpr uint32_t kNttBatch = 16;
+// issued before the first is used (8: measured faster than 16, which took
+// the passes past 128 VGPRs).
+constexpr uint32_t kNttBatch = 8;
 
 // Pass A, N2 = 2^LOGM: grid (N1 / kNttCols, vectors).  Thread t handles
 // column c0 + t % kNttCols, rows n2 = t / kNttCols + j * (kNttThreads / kNttCols).
@@ -193,27 +205,31 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
   constexpr uint32_t B = PER < kNttBatch ? PER : kNttBatch, RSTEP = kNttThreads / kNttCols;
   extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * PM);
-  stage_twiddles(tw, P.dft_a, LOGM);
+  const uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps;
+  const NttSet S = P.sets[set];
+  stage_twiddles(tw, S.dft_a, LOGM);
   const uint32_t N1 = 1u << P.log_n1, c = threadIdx.x % kNttCols, r = threadIdx.x / kNttCols;
   const uint32_t n1 = blockIdx.x * kNttCols + c;
   const uint64_t v = blockIdx.y;
-  const double q = P.q, qinv = P.qinv;
-#pragma unroll
+  const uint64_t in_off = set * P.in_set_stride + lv * P.in_stride;
+  const double q = S.q, qinv = S.qinv;
+  // batches one after the other (not unrolled): fewer registers, more waves
+#pragma unroll 1
   for (uint32_t b0 = 0; b0 < PER; b0 += B) {
     double x[B];
     if (P.load == kLoadF64) {
-      const double *in = (const double *)P.in + v * P.in_stride + n1;
+      const double *in = (const double *)P.in + in_off + n1;
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) x[j] = in[(size_t)N1 * (r + (b0 + j) * RSTEP)];
     } else {
-      const uint64_t *in = (const uint64_t *)P.in + v * P.in_stride + n1;
+      const uint64_t *in = (const uint64_t *)P.in + in_off + n1;
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) x[j] = to_f64(in[(size_t)N1 * (r + (b0 + j) * RSTEP)]);
     }
-    if (P.pre) {
+    if (S.pre) {
       Tw t[B];
 #pragma unroll
-      for (uint32_t j = 0; j < B; ++j) t[j] = P.pre[n1 + N1 * (r + (b0 + j) * RSTEP)];
+      for (uint32_t j = 0; j < B; ++j) t[j] = S.pre[n1 + N1 * (r + (b0 + j) * RSTEP)];
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) x[j] = mul_tw(x[j], t[j], q);
     } else {
@@ -225,11 +241,11 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
   }
   lds_dft<LOGM>(xs, tw, q, qinv);
   double *tmp = P.tmp + v * ((uint64_t)N1 * M) + n1;
-#pragma unroll
+#pragma unroll 1
   for (uint32_t b0 = 0; b0 < PER; b0 += B) {
     Tw t[B];
 #pragma unroll
-    for (uint32_t j = 0; j < B; ++j) t[j] = P.mid[(size_t)(r + (b0 + j) * RSTEP) * N1 + n1];
+    for (uint32_t j = 0; j < B; ++j) t[j] = S.mid[(size_t)(r + (b0 + j) * RSTEP) * N1 + n1];
 #pragma unroll
     for (uint32_t j = 0; j < B; ++j) {
       const uint32_t k2 = r + (b0 + j) * RSTEP;
@@ -246,10 +262,12 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
   constexpr uint32_t B = PER < kNttBatch ? PER : kNttBatch, RSTEP = kNttThreads / kNttCols;
   extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * PM);
-  stage_twiddles(tw, P.dft_b, LOGM);
+  const uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps;
+  const NttSet S = P.sets[set];
+  stage_twiddles(tw, S.dft_b, LOGM);
   const uint32_t N2 = 1u << P.log_n2, r0 = blockIdx.x * kNttCols;
   const uint64_t v = blockIdx.y;
-  const double q = P.q, qinv = P.qinv;
+  const double q = S.q, qinv = S.qinv;
   const double *tmp = P.tmp + v * ((uint64_t)N2 * M) + (size_t)r0 * M;
 #pragma unroll
   for (uint32_t b0 = 0; b0 < PER; b0 += B) {
@@ -269,27 +287,27 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
     double y[B];
 #pragma unroll
     for (uint32_t j = 0; j < B; ++j) y[j] = xs[c * PM + pidx(r + (b0 + j) * RSTEP)];
-    if (P.post) {
+    if (S.post) {
       Tw t[B];
 #pragma unroll
-      for (uint32_t j = 0; j < B; ++j) t[j] = P.post[k2 + (size_t)N2 * (r + (b0 + j) * RSTEP)];
+      for (uint32_t j = 0; j < B; ++j) t[j] = S.post[k2 + (size_t)N2 * (r + (b0 + j) * RSTEP)];
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) y[j] = mul_tw(y[j], t[j], q);
     }
     if (P.store == kStoreF64) {
-      double *out = (double *)P.out + v * P.out_stride + k2;
+      double *out = (double *)P.out + set * P.out_set_stride + lv * P.out_stride + k2;
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) out[(size_t)N2 * (r + (b0 + j) * RSTEP)] = reduce(y[j], q, qinv);
     } else {
       if (P.store == kStoreRescale) {
-        const uint64_t *base = P.base + v * P.base_stride + k2;
+        const uint64_t *base = P.base + set * P.base_set_stride + lv * P.base_stride + k2;
         uint64_t bv[B];
 #pragma unroll
         for (uint32_t j = 0; j < B; ++j) bv[j] = base[(size_t)N2 * (r + (b0 + j) * RSTEP)];
 #pragma unroll
-        for (uint32_t j = 0; j < B; ++j) y[j] = mul_tw(to_f64(bv[j]) - y[j], P.inv, q);
+        for (uint32_t j = 0; j < B; ++j) y[j] = mul_tw(to_f64(bv[j]) - y[j], S.inv, q);
       }
-      uint64_t *out = (uint64_t *)P.out + v * P.out_stride + k2;
+      uint64_t *out = (uint64_t *)P.out + set * P.out_set_stride + lv * P.out_stride + k2;
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) out[(size_t)N2 * (r + (b0 + j) * RSTEP)] = to_u64(canonical(y[j], q, qinv));
     }

@@ -1,0 +1,368 @@
+// Hoisted baby-step rotations: the step that produces the hot path's input
+// ciphertexts.  A linear layer's inputs A_i are the packed input rotated by
+// the packing layout's baby steps (paper Sec. 2, "Homomorphic Operations":
+// Rot cyclically shifts the slots; Sec. 4.2: the A_i are prepared according
+// to the packing layout).  Rot by r slots is the automorphism
+// sigma_g: a(X) -> a(X^g), g = 5^r mod 2N, on both polynomials, then a key
+// switch of the second one from sigma_g(s) back to s, by RNS digits (digit j
+// = the coefficients of c1 mod q_j, in [0, q_j)), over the data moduli and
+// one special prime P, with a rounded division by P at the end.
+//
+// In the NTT domain a_hat_k = a(psi^(2k+1)), the automorphism is the slot
+// gather (sigma a)_hat[k] = a_hat[pi(k)], pi(k) = k g + (g - 1) / 2 mod N.
+// Per call (one input ciphertext, several rotations):
+//   1. digits, once (hoisting): D_j = INTT_{q_j}(c1_j) and
+//      Dhat[j][m] = NTT_m(D_j mod m) for every modulus m of q_0 .. q_{L-1}, P;
+//   2. per rotation, the key-switch inner product in the pi^-1 frame:
+//      u'_p[m][i] = sum_j Dhat[j][m][i] * K'[j][p][m][i]  mod m, where the
+//      library's key layout holds K'[j][p][m][i] = ksk_hat[j][p][m][pi^-1(i)],
+//      so that no digit is gathered;
+//   3. the division by P with rounding (the rescale of the chain
+//      q_0 .. q_{L-1}, P): v' = round(u' / P);
+//   4. the gather back: out_0[k] = c0[pi(k)] + v'_0[pi(k)],
+//      out_1[k] = v'_1[pi(k)], exact because the automorphism permutes the
+//      coefficients up to sign and the rounding division is odd-symmetric
+//      (P is odd: no ties).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "fiona.h"
+#include "fiona_ctx.hpp"
+#include "modarith.hpp"
+#include "ntt_host.hpp"
+
+using namespace fiona_host;
+
+namespace fiona {
+
+constexpr uint32_t kKsTile = 64;    // coefficients per workgroup of the inner product (one per lane)
+constexpr uint32_t kKsWaves = 8;    // wavefronts per workgroup; rotations are dealt out to them
+
+// Step 2.  Workgroup = (modulus m, tile of 64 coefficients).  The L digits of
+// the tile are staged in LDS as radix-2^25 digit pairs; each wavefront then
+// takes rotations r = wave, wave + kKsWaves, ..., loads the 2 L key words of
+// each lane in batches of JB digits (both polynomials), and accumulates the
+// exact products (modarith.hpp), reduced once per output.  Padding terms of a
+// batch read the zero row and repeat a real key address.
+template <uint32_t JB>
+__global__ void __launch_bounds__(kKsWaves * 64) ks_inner_kernel(const uint64_t *__restrict__ dhat,
+                                                                  const uint64_t *__restrict__ keys,
+                                                                  uint64_t *__restrict__ u,
+                                                                  const LimbConst *__restrict__ limbs, uint32_t N,
+                                                                  uint32_t L, uint32_t n_rot) {
+  extern __shared__ uint2 ks_lds[];   // [L + 1][64]: digits of Dhat[j][m] at this tile, then a zero row
+  uint2 *xs = ks_lds;
+  const uint32_t tiles = N / kKsTile;
+  const uint32_t m = blockIdx.x / tiles, t = blockIdx.x - m * tiles;
+  const uint32_t lane = threadIdx.x & 63u, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t k = t * kKsTile + lane;
+  const uint32_t M = L + 1;
+  for (uint32_t j = wave; j < L; j += kKsWaves) {
+    const uint64_t x = __builtin_nontemporal_load(dhat + ((size_t)j * M + m) * N + k);
+    xs[j * 64 + lane] = make_uint2(lo_digit(x), hi_digit(x));
+  }
+  if (wave == 0) xs[L * 64 + lane] = make_uint2(0, 0);
+  __syncthreads();
+  const LimbConst lc = limbs[m];
+  const size_t poly = (size_t)M * N;           // words between the two polynomials of a digit
+  const size_t rot_words = (size_t)L * 2 * poly;
+  for (uint32_t r = wave; r < n_rot; r += kKsWaves) {
+    const uint64_t *kr = keys + (size_t)r * rot_words + (size_t)m * N + k;
+    Acc a0, a1;
+    acc_zero(a0);
+    acc_zero(a1);
+    for (uint32_t j0 = 0; j0 < L; j0 += JB) {
+      uint64_t w0[JB], w1[JB];
+#pragma unroll
+      for (uint32_t b = 0; b < JB; ++b) {
+        const uint32_t j = j0 + b < L ? j0 + b : L - 1;
+        w0[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly);
+        w1[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly + poly);
+      }
+#pragma unroll
+      for (uint32_t b = 0; b < JB; ++b) {
+        const uint32_t row = j0 + b < L ? j0 + b : L;
+        const uint2 x = xs[row * 64 + lane];
+        mac(a0, x.x, x.y, (uint32_t)w0[b], (uint32_t)(w0[b] >> 32));
+        mac(a1, x.x, x.y, (uint32_t)w1[b], (uint32_t)(w1[b] >> 32));
+      }
+    }
+    uint64_t *ur = u + ((size_t)r * 2 * M + m) * N + k;
+    __builtin_nontemporal_store(finish(a0, 0, lc), ur);
+    __builtin_nontemporal_store(finish(a1, 0, lc), ur + poly);
+  }
+}
+
+// Step 4, one rotation.  Workgroup = (limb, polynomial, tile of 256); the
+// limbs are dealt out so that limb l runs on the XCD blockIdx % 8 == l % 8,
+// which then holds that limb's gather sources in its L2.
+constexpr uint32_t kGatherTile = 256;
+
+__global__ void __launch_bounds__(kGatherTile) gather_kernel(const uint64_t *__restrict__ c0,
+                                                             const uint64_t *__restrict__ v,
+                                                             uint64_t *__restrict__ out,
+                                                             const LimbConst *__restrict__ limbs, uint32_t N,
+                                                             uint32_t L, uint32_t g) {
+  const uint32_t tiles = N / kGatherTile;
+  const uint32_t xcd = blockIdx.x & 7u, local = blockIdx.x >> 3;
+  const uint32_t limb = xcd + 8u * (local / (2 * tiles));
+  if (limb >= L) return;
+  const uint32_t rest = local % (2 * tiles), p = rest / tiles, t = rest - p * tiles;
+  const uint32_t k = t * kGatherTile + threadIdx.x;
+  const uint32_t src = (k * g + (g - 1) / 2) & (N - 1);   // pi(k); N divides 2^32
+  const size_t row = ((size_t)p * L + limb) * N;
+  uint64_t y = v[row + src];
+  if (p == 0) {
+    const uint64_t q = limbs[limb].q;
+    y += c0[(size_t)limb * N + src];
+    y = y >= q ? y - q : y;
+  }
+  out[row + k] = y;
+}
+
+// The library's key layout: K'[row][i] = K[row][pi^-1(i)] for every row of N
+// words, pi^-1(i) = (i - (g - 1) / 2) g^-1 mod N.
+__global__ void __launch_bounds__(256) key_layout_kernel(const uint64_t *__restrict__ key,
+                                                         uint64_t *__restrict__ out, uint32_t N, uint32_t rows,
+                                                         uint32_t g, uint32_t ginv) {
+  const uint32_t row = blockIdx.y;
+  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (row >= rows || i >= N) return;
+  const uint32_t src = ((i - (g - 1) / 2) * ginv) & (N - 1);
+  out[(size_t)row * N + i] = key[(size_t)row * N + src];
+}
+
+}  // namespace fiona
+
+struct fiona_rotator {
+  const fiona_ctx *ctx = nullptr;
+  fiona_ctx *ext = nullptr;            // q_0 .. q_{L-1}, P
+  fiona_rescaler *down = nullptr;      // the division by P: a rescale of the extended chain
+  uint32_t N = 0, L = 0, log_n1 = 0, log_n2 = 0, max_rot = 0;
+  uint64_t P = 0;
+  int device = -1;
+  void *dev = nullptr;
+  const NttSet *inv_sets = nullptr;    // [L] inverse transforms of q_0 .. q_{L-1}
+  const NttSet *fwd_sets = nullptr;    // [L + 1] forward transforms of q_0 .. q_{L-1}, P
+  const fiona::LimbConst *limbs = nullptr;   // [L + 1] on the device
+  uint64_t *D = nullptr;               // [L][N] digits
+  uint64_t *Dhat = nullptr;            // [L][L + 1][N]
+  double *T = nullptr;                 // NTT intermediates, L (L + 1) vectors
+  uint64_t *U = nullptr;               // [max_rot][2][L + 1][N]
+  uint64_t *Y = nullptr;               // [max_rot][2][L][N]
+};
+
+namespace {
+
+size_t round256(size_t x) { return (x + 255) / 256 * 256; }
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uint64_t *psi, uint32_t max_rot,
+                         fiona_rotator **out) {
+  if (!out) return FIONA_ERR_ARG;
+  *out = nullptr;
+  if (!ctx || max_rot == 0) return FIONA_ERR_ARG;
+  const uint32_t N = ctx->N, L = ctx->L;
+  uint32_t logN = 0;
+  while ((1u << logN) < N) ++logN;
+  if ((1u << logN) != N || logN < 8 || logN > 17 || L < 1 || L + 1 > FIONA_MAX_L) return FIONA_ERR_UNSUPPORTED;
+  if ((size_t)L * (L + 1) > 65535 || 2ull * max_rot > 65535) return FIONA_ERR_UNSUPPORTED;
+  const uint64_t P = special_prime;
+  if (P <= (1ull << FIONA_SCALE_BITS) || P >= (1ull << FIONA_MODULUS_BITS) || (P - 1) % (2ull * N) != 0)
+    return FIONA_ERR_UNSUPPORTED;
+  std::vector<uint64_t> mods(ctx->q.begin(), ctx->q.end());
+  for (uint64_t q : mods)
+    if (q == P) return FIONA_ERR_UNSUPPORTED;
+  mods.push_back(P);
+  std::vector<uint64_t> roots(L + 1);
+  for (uint32_t i = 0; i <= L; ++i) {
+    const uint64_t q = mods[i];
+    if ((q - 1) % (2ull * N) != 0) return FIONA_ERR_UNSUPPORTED;
+    roots[i] = psi ? psi[i] % q : default_psi(N, q);
+    if (roots[i] == 0 || powmod_h(roots[i], N, q) != q - 1) return FIONA_ERR_UNSUPPORTED;
+  }
+  fiona_rotator *R = new (std::nothrow) fiona_rotator;
+  if (!R) return FIONA_ERR_NOMEM;
+  R->ctx = ctx;
+  R->N = N;
+  R->L = L;
+  R->P = P;
+  R->log_n1 = (logN + 1) / 2;
+  R->log_n2 = logN / 2;
+  R->max_rot = max_rot;
+  int rc = fiona_ctx_create(N, L + 1, mods.data(), &R->ext);
+  if (rc == FIONA_OK) rc = fiona_rescaler_create(R->ext, roots.data(), max_rot, &R->down);
+  if (rc != FIONA_OK) {
+    fiona_rotator_destroy(R);
+    return rc;
+  }
+  try {
+    TableImage img;
+    for (uint32_t j = 0; j < L; ++j) img.add(make_tables(R->log_n1, R->log_n2, mods[j], roots[j], true), mods[j]);
+    for (uint32_t i = 0; i <= L; ++i) img.add(make_tables(R->log_n1, R->log_n2, mods[i], roots[i], false), mods[i]);
+    const size_t img_bytes = img.bytes();
+    const size_t limb_bytes = round256((L + 1) * sizeof(fiona::LimbConst));
+    const size_t d_bytes = round256((size_t)L * N * 8);
+    const size_t dhat_bytes = round256((size_t)L * (L + 1) * N * 8);
+    const size_t t_bytes = round256((size_t)L * (L + 1) * N * 8);
+    const size_t u_bytes = round256((size_t)max_rot * 2 * (L + 1) * N * 8);
+    const size_t y_bytes = round256((size_t)max_rot * 2 * L * N * 8);
+    if (hipGetDevice(&R->device) != hipSuccess) {
+      fiona_rotator_destroy(R);
+      return FIONA_ERR_HIP;
+    }
+    const size_t total = img_bytes + limb_bytes + d_bytes + dhat_bytes + t_bytes + u_bytes + y_bytes;
+    if (hipMalloc(&R->dev, total) != hipSuccess) {
+      R->dev = nullptr;
+      fiona_rotator_destroy(R);
+      return FIONA_ERR_NOMEM;
+    }
+    const NttSet *sets = img.upload(R->dev);
+    char *p = (char *)R->dev + img_bytes;
+    if (!sets || hipMemcpy(p, R->ext->limbs.data(), (L + 1) * sizeof(fiona::LimbConst), hipMemcpyHostToDevice) !=
+                     hipSuccess) {
+      fiona_rotator_destroy(R);
+      return FIONA_ERR_HIP;
+    }
+    R->inv_sets = sets;
+    R->fwd_sets = sets + L;
+    R->limbs = (const fiona::LimbConst *)p;
+    p += limb_bytes;
+    R->D = (uint64_t *)p;
+    p += d_bytes;
+    R->Dhat = (uint64_t *)p;
+    p += dhat_bytes;
+    R->T = (double *)p;
+    p += t_bytes;
+    R->U = (uint64_t *)p;
+    p += u_bytes;
+    R->Y = (uint64_t *)p;
+    const int ks_smem = (int)((L + 1) * 64 * sizeof(uint2));
+    if (!allow_smem() ||
+        hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            ks_smem) != hipSuccess ||
+        hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            ks_smem) != hipSuccess) {
+      fiona_rotator_destroy(R);
+      return FIONA_ERR_HIP;
+    }
+  } catch (...) {
+    fiona_rotator_destroy(R);
+    return FIONA_ERR_NOMEM;
+  }
+  *out = R;
+  return FIONA_OK;
+}
+
+void fiona_rotator_destroy(fiona_rotator *R) {
+  if (!R) return;
+  if (R->dev) (void)hipFree(R->dev);
+  fiona_rescaler_destroy(R->down);
+  fiona_ctx_destroy(R->ext);
+  delete R;
+}
+
+uint64_t fiona_rotation_key_words(const fiona_rotator *R) {
+  return R ? (uint64_t)R->L * 2 * (R->L + 1) * R->N : 0;
+}
+
+int fiona_rotation_key_layout(const fiona_rotator *R, uint32_t galois, const uint64_t *key, uint64_t *key_out,
+                              hipStream_t stream) {
+  if (!R || !key || !key_out) return FIONA_ERR_ARG;
+  const uint32_t N = R->N;
+  if ((galois & 1u) == 0 || galois >= 2 * N) return FIONA_ERR_ARG;
+  if (((uintptr_t)key | (uintptr_t)key_out) & 7u) return FIONA_ERR_ALIGN;
+  const size_t words = fiona_rotation_key_words(R);
+  if (overlap(key, words * 8, key_out, words * 8)) return FIONA_ERR_ALIAS;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != R->device) return FIONA_ERR_ARG;
+  uint32_t ginv = 1;   // g^-1 mod N by Newton's iteration (g odd, N a power of two)
+  for (int i = 0; i < 5; ++i) ginv *= 2u - galois * ginv;
+  const uint32_t rows = R->L * 2 * (R->L + 1);
+  hipLaunchKernelGGL(fiona::key_layout_kernel, dim3(N / 256, rows), dim3(256), 0, stream, key, key_out, N, rows,
+                     galois, ginv & (N - 1));
+  return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
+}
+
+int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_rot, const uint32_t *galois,
+                         const uint64_t *keys, uint64_t *out_cts, hipStream_t stream) {
+  if (!R) return FIONA_ERR_ARG;
+  if (n_rot == 0) return FIONA_OK;
+  if (!ct || !galois || !keys || !out_cts || n_rot > R->max_rot) return FIONA_ERR_ARG;
+  const uint32_t N = R->N, L = R->L;
+  for (uint32_t r = 0; r < n_rot; ++r)
+    if ((galois[r] & 1u) == 0 || galois[r] >= 2 * N) return FIONA_ERR_ARG;
+  if (((uintptr_t)ct | (uintptr_t)keys | (uintptr_t)out_cts) & 7u) return FIONA_ERR_ALIGN;
+  const size_t ct_bytes = (size_t)2 * L * N * 8, out_bytes = (size_t)n_rot * ct_bytes;
+  const size_t key_bytes = (size_t)n_rot * fiona_rotation_key_words(R) * 8;
+  if (overlap(out_cts, out_bytes, ct, ct_bytes) || overlap(out_cts, out_bytes, keys, key_bytes))
+    return FIONA_ERR_ALIAS;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != R->device) return FIONA_ERR_ARG;
+  const uint32_t M = L + 1;
+
+  // 1. digits of c1, once: D_j = INTT_{q_j}(c1_j), then Dhat[j][m] = NTT_m(D_j)
+  NttPass A{};
+  A.sets = R->inv_sets;
+  A.vps = 1;
+  A.log_n1 = R->log_n1;
+  A.log_n2 = R->log_n2;
+  A.in = ct + (size_t)L * N;
+  A.in_set_stride = N;
+  A.tmp = R->T;
+  A.out = R->D;
+  A.out_set_stride = N;
+  A.load = fiona::kLoadU64;
+  A.store = fiona::kStoreU64;
+  launch_transform(R->log_n1, R->log_n2, L, stream, A);
+  NttPass B{};
+  B.sets = R->fwd_sets;
+  B.vps = L;
+  B.log_n1 = R->log_n1;
+  B.log_n2 = R->log_n2;
+  B.in = R->D;
+  B.in_stride = N;
+  B.tmp = R->T;
+  B.out = R->Dhat;
+  B.out_stride = (size_t)M * N;
+  B.out_set_stride = N;
+  B.load = fiona::kLoadU64;
+  B.store = fiona::kStoreU64;
+  launch_transform(R->log_n1, R->log_n2, L * M, stream, B);
+
+  // 2. the inner products of every rotation, in the pi^-1 frame
+  const dim3 ks_grid(M * (N / fiona::kKsTile));
+  const size_t ks_smem = (size_t)M * 64 * sizeof(uint2);
+  if (L <= 8)
+    hipLaunchKernelGGL(fiona::ks_inner_kernel<8>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat, keys,
+                       R->U, R->limbs, N, L, n_rot);
+  else
+    hipLaunchKernelGGL(fiona::ks_inner_kernel<16>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat,
+                       keys, R->U, R->limbs, N, L, n_rot);
+  if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
+
+  // 3. the rounded division by P
+  const int rc = fiona_rescale(R->down, R->U, n_rot, R->Y, stream);
+  if (rc != FIONA_OK) return rc;
+
+  // 4. the gather back, with c0 added to the first polynomial
+  const uint32_t gather_blocks = 8 * ((L + 7) / 8) * 2 * (N / fiona::kGatherTile);
+  for (uint32_t r = 0; r < n_rot; ++r)
+    hipLaunchKernelGGL(fiona::gather_kernel, dim3(gather_blocks), dim3(fiona::kGatherTile), 0, stream, ct,
+                       R->Y + (size_t)r * 2 * L * N, out_cts + (size_t)r * 2 * L * N, R->limbs, N, L, galois[r]);
+  return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
+}
+
+}  // extern "C"

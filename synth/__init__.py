@@ -60,6 +60,7 @@ TAG_PICK = 7      # pool entry picked by a group
 TAG_FLIP = 8      # global sign flip of a pooled group
 TAG_SAMPLE = 9    # sampled positions for checks at full size
 TAG_CT = 10        # stand-alone ciphertexts (e.g. the outputs a rescale receives)
+TAG_KEY = 11       # rotation keys
 
 SIGN_T1 = (35 << 64) // 100  # u < T1 -> +1
 SIGN_T2 = (70 << 64) // 100  # T1 <= u < T2 -> -1, else 0

@@ -75,6 +75,18 @@ def fill_cts(layer: Layer, t, n_ct: int) -> None:
         raise RuntimeError("synth_fill_uniform failed (%d)" % rc)
 
 
+def fill_rows(t, n_rows: int, moduli, N: int, seed: int, tag: int) -> None:
+    """t: device tensor of >= n_rows*N 8-byte elements -> rows of N uniform residues,
+    row r modulo moduli[r % len(moduli)], value at flat index r*N + k as in
+    synth.uniform_mod_np(seed, tag, r*N + k, q)."""
+    assert t.is_cuda and t.is_contiguous() and t.element_size() == 8 and t.numel() >= n_rows * N
+    m = (ctypes.c_uint64 * len(moduli))(*[int(q) for q in moduli])
+    rc = lib().synth_fill_uniform(t.data_ptr(), n_rows, len(moduli), N, seed, tag, ctypes.cast(m, ctypes.c_void_p),
+                                  _stream())
+    if rc != 0:
+        raise RuntimeError("synth_fill_uniform failed (%d)" % rc)
+
+
 def fill_pts(layer: Layer, t, pitch: int = 0) -> None:
     """t: device tensor -> this layer's plaintext table, plaintext p at word p * pitch
     (pitch 0 = L*N, packed rows); t needs (n_pt-1)*pitch + L*N 8-byte elements."""

@@ -296,3 +296,20 @@ def test_rescaler_validation_without_device():
     L.fiona_rescale.restype = ctypes.c_int
     L.fiona_rescale.argtypes = [ctypes.c_void_p] * 2 + [ctypes.c_uint32] + [ctypes.c_void_p] * 2
     assert L.fiona_rescale(None, None, 1, None, None) == -1
+
+
+def test_rotator_validation():
+    """fiona_rotator_create checks its arguments before touching the device."""
+    N, L = 256, 2
+    ps = synth.ntt_primes(N, L + 1)
+    ctx = fiona.Ctx(N, L, ps[:L])
+    for P, max_rot, status in [(ps[L] + 2, 1, -3), (ps[0], 1, -3), (ps[L], 0, -1), (1 << 50, 1, -3),
+                               (3, 1, -3)]:
+        with pytest.raises(fiona.FionaError) as e:
+            fiona.Rotator(ctx, P, max_rot)
+        assert e.value.status == status
+    small = fiona.Ctx(128, L, synth.ntt_primes(128, L))
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.Rotator(small, synth.ntt_primes(128, L + 1)[L], 1)
+    assert e.value.status == -3
+    assert fiona.lib().fiona_rotation_key_words(None) == 0
