@@ -163,6 +163,8 @@ enum NttStore : uint32_t {
   kStoreU64 = 0,      // the transform, residues in [0, q) as uint64
   kStoreF64 = 1,      // the transform, centred residues as doubles
   kStoreRescale = 2,  // (base - transform) * inv mod q, in [0, q) as uint64
+  kStoreRescaleT = 3, // the same, plus add[k] for the first add_count vectors of each set, stored
+                      // transposed: element k2 + N2 k1 at k2 N1 + k1
 };
 
 // One modulus of a pass and its tables.
@@ -187,9 +189,10 @@ struct NttPass {
   void *out;             // pass B output
   const uint64_t *base;  // kStoreRescale: residues in [0, q)
   const NttSet *sets;    // device array, one entry per set
+  const uint64_t *add;   // kStoreRescaleT: residues in [0, q), set s at add + s * add_set_stride
   uint64_t in_stride, out_stride, base_stride;
-  uint64_t in_set_stride, out_set_stride, base_set_stride;
-  uint32_t vps, log_n1, log_n2, load, store;
+  uint64_t in_set_stride, out_set_stride, base_set_stride, add_set_stride;
+  uint32_t vps, log_n1, log_n2, load, store, add_count;
 };
 
 // Global loads and stores go in batches of up to kNttBatch per thread, all
@@ -282,6 +285,10 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
   }
   lds_dft<LOGM>(xs, tw, q, qinv);
   const uint32_t c = threadIdx.x % kNttCols, r = threadIdx.x / kNttCols, k2 = r0 + c;
+  const bool transposed = P.store == kStoreRescaleT;
+  const bool rescale = P.store == kStoreRescale || transposed;
+  const uint64_t *base = rescale ? P.base + set * P.base_set_stride + lv * P.base_stride + k2 : nullptr;
+  const uint64_t *add = transposed && lv < P.add_count ? P.add + set * P.add_set_stride + k2 : nullptr;
 #pragma unroll
   for (uint32_t b0 = 0; b0 < PER; b0 += B) {
     double y[B];
@@ -298,18 +305,45 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
       double *out = (double *)P.out + set * P.out_set_stride + lv * P.out_stride + k2;
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) out[(size_t)N2 * (r + (b0 + j) * RSTEP)] = reduce(y[j], q, qinv);
-    } else {
-      if (P.store == kStoreRescale) {
-        const uint64_t *base = P.base + set * P.base_set_stride + lv * P.base_stride + k2;
-        uint64_t bv[B];
+      continue;
+    }
+    if (rescale) {
+      uint64_t bv[B];
 #pragma unroll
-        for (uint32_t j = 0; j < B; ++j) bv[j] = base[(size_t)N2 * (r + (b0 + j) * RSTEP)];
+      for (uint32_t j = 0; j < B; ++j) bv[j] = base[(size_t)N2 * (r + (b0 + j) * RSTEP)];
 #pragma unroll
-        for (uint32_t j = 0; j < B; ++j) y[j] = mul_tw(to_f64(bv[j]) - y[j], S.inv, q);
+      for (uint32_t j = 0; j < B; ++j) y[j] = mul_tw(to_f64(bv[j]) - y[j], S.inv, q);
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) y[j] = canonical(y[j], q, qinv);
+    if (add) {
+      uint64_t av[B];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) av[j] = add[(size_t)N2 * (r + (b0 + j) * RSTEP)];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) {
+        const double z = y[j] + to_f64(av[j]);
+        y[j] = z >= q ? z - q : z;
       }
+    }
+    if (transposed) {
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) xs[c * PM + pidx(r + (b0 + j) * RSTEP)] = y[j];
+    } else {
       uint64_t *out = (uint64_t *)P.out + set * P.out_set_stride + lv * P.out_stride + k2;
 #pragma unroll
-      for (uint32_t j = 0; j < B; ++j) out[(size_t)N2 * (r + (b0 + j) * RSTEP)] = to_u64(canonical(y[j], q, qinv));
+      for (uint32_t j = 0; j < B; ++j) out[(size_t)N2 * (r + (b0 + j) * RSTEP)] = to_u64(y[j]);
+    }
+  }
+  if (transposed) {   // uniform over the workgroup
+    // each quarter wave stores kNttCols consecutive k1 of one row k2
+    __syncthreads();
+    const uint32_t cc = threadIdx.x / kNttCols, kk = threadIdx.x % kNttCols;
+    uint64_t *out = (uint64_t *)P.out + set * P.out_set_stride + lv * P.out_stride + (size_t)(r0 + cc) * M;
+#pragma unroll
+    for (uint32_t j = 0; j < PER; ++j) {
+      const uint32_t k1 = kk + j * kNttCols;
+      out[k1] = to_u64(xs[cc * PM + pidx(k1)]);
     }
   }
 }

@@ -18,11 +18,10 @@
 //      library's key layout holds K'[j][p][m][i] = ksk_hat[j][p][m][pi^-1(i)],
 //      so that no digit is gathered;
 //   3. the division by P with rounding (the rescale of the chain
-//      q_0 .. q_{L-1}, P): v' = round(u' / P);
-//   4. the gather back: out_0[k] = c0[pi(k)] + v'_0[pi(k)],
-//      out_1[k] = v'_1[pi(k)], exact because the automorphism permutes the
-//      coefficients up to sign and the rounding division is odd-symmetric
-//      (P is odd: no ties).
+//      q_0 .. q_{L-1}, P): v' = round(u' / P), with c0 added to v'_0;
+//   4. the gather back: out_0[k] = (c0 + v'_0)[pi(k)], out_1[k] = v'_1[pi(k)],
+//      exact because the automorphism permutes the coefficients up to sign
+//      and the rounding division is odd-symmetric (P is odd: no ties).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -34,6 +33,7 @@
 #include "fiona_ctx.hpp"
 #include "modarith.hpp"
 #include "ntt_host.hpp"
+#include "rescale_internal.hpp"
 
 using namespace fiona_host;
 
@@ -91,37 +91,56 @@ __global__ void __launch_bounds__(kKsWaves * 64) ks_inner_kernel(const uint64_t 
         mac(a1, x.x, x.y, (uint32_t)w1[b], (uint32_t)(w1[b] >> 32));
       }
     }
-    uint64_t *ur = u + ((size_t)r * 2 * M + m) * N + k;
+    uint64_t *ur = u + ((size_t)r * M + m) * N + k;   // u: [2][n_rot][L + 1][N]
     __builtin_nontemporal_store(finish(a0, 0, lc), ur);
-    __builtin_nontemporal_store(finish(a1, 0, lc), ur + poly);
+    __builtin_nontemporal_store(finish(a1, 0, lc), ur + (size_t)n_rot * poly);
   }
 }
 
-// Step 4, one rotation.  Workgroup = (limb, polynomial, tile of 256); the
-// limbs are dealt out so that limb l runs on the XCD blockIdx % 8 == l % 8,
-// which then holds that limb's gather sources in its L2.
-constexpr uint32_t kGatherTile = 256;
+// Step 4.  The division by P leaves every limb of v' transposed: element
+// k = k2 + N2 k1 at k2 N1 + k1 (N = N1 N2, the four-step split).  With
+// d = d_lo + N2 d_hi and A = (g d_lo + c) mod N, pi(d) = k2 + N2 k1 with
+// k2 = A mod N2 and k1 = (A / N2 + g d_hi) mod N1: the 16 destinations
+// d_lo .. d_lo + 15 of every d_hi read the 16 source rows k2 = A mod N2.  A
+// workgroup (vector, limb, 16 consecutive d_lo) loads those rows whole
+// (contiguous N1 words each) into LDS, then stores its destinations as runs
+// of 16 words.  The Galois elements of up to kGatherMaxRot rotations ride in
+// the arguments.
+constexpr uint32_t kGatherThreads = 256;
+constexpr uint32_t kGatherCols = 16;
+constexpr uint32_t kGatherMaxRot = 256;
 
-__global__ void __launch_bounds__(kGatherTile) gather_kernel(const uint64_t *__restrict__ c0,
-                                                             const uint64_t *__restrict__ v,
-                                                             uint64_t *__restrict__ out,
-                                                             const LimbConst *__restrict__ limbs, uint32_t N,
-                                                             uint32_t L, uint32_t g) {
-  const uint32_t tiles = N / kGatherTile;
-  const uint32_t xcd = blockIdx.x & 7u, local = blockIdx.x >> 3;
-  const uint32_t limb = xcd + 8u * (local / (2 * tiles));
-  if (limb >= L) return;
-  const uint32_t rest = local % (2 * tiles), p = rest / tiles, t = rest - p * tiles;
-  const uint32_t k = t * kGatherTile + threadIdx.x;
-  const uint32_t src = (k * g + (g - 1) / 2) & (N - 1);   // pi(k); N divides 2^32
-  const size_t row = ((size_t)p * L + limb) * N;
-  uint64_t y = v[row + src];
-  if (p == 0) {
-    const uint64_t q = limbs[limb].q;
-    y += c0[(size_t)limb * N + src];
-    y = y >= q ? y - q : y;
+struct GatherArgs {
+  uint32_t g[kGatherMaxRot];
+};
+
+__global__ void __launch_bounds__(kGatherThreads) gather_kernel(const uint64_t *__restrict__ vt,
+                                                                uint64_t *__restrict__ out, uint32_t log_n1,
+                                                                uint32_t log_n2, uint32_t L, uint32_t n_rot,
+                                                                uint32_t r0, uint32_t nr, const GatherArgs G) {
+  extern __shared__ uint64_t gather_lds[];   // [kGatherCols][N1 + 1]
+  const uint32_t N1 = 1u << log_n1, N2 = 1u << log_n2, N = N1 * N2, PM = N1 + 1;
+  const uint32_t blocks = N2 / kGatherCols;
+  const uint32_t blk = blockIdx.x % blocks, rest = blockIdx.x / blocks;
+  const uint32_t limb = rest % L, lv = rest / L;   // lv = p nr + local rotation
+  const uint32_t p = lv / nr, rl = lv - p * nr, r = r0 + rl;
+  const uint32_t g = G.g[rl], c = (g - 1) / 2;
+  const uint32_t o0 = blk * kGatherCols;
+  const uint64_t *src = vt + ((size_t)(p * n_rot + r) * L + limb) * N;
+  for (uint32_t w = threadIdx.x; w < kGatherCols * N1; w += kGatherThreads) {
+    const uint32_t col = w >> log_n1, row = w & (N1 - 1);
+    const uint32_t k2 = (g * (o0 + col) + c) & (N2 - 1);   // A mod N2 (N2 divides 2^32)
+    gather_lds[col * PM + row] = src[(size_t)k2 * N1 + row];
   }
-  out[row + k] = y;
+  __syncthreads();
+  const uint32_t col = threadIdx.x % kGatherCols;
+  const uint32_t A = (g * (o0 + col) + c) & (N - 1);
+  const uint32_t hi = A >> log_n2;
+  uint64_t *dst = out + ((size_t)(r * 2 + p) * L + limb) * N + o0 + col;
+  for (uint32_t d_hi = threadIdx.x / kGatherCols; d_hi < N1; d_hi += kGatherThreads / kGatherCols) {
+    const uint32_t k1 = (hi + g * d_hi) & (N1 - 1);
+    dst[(size_t)d_hi * N2] = gather_lds[col * PM + k1];
+  }
 }
 
 // The library's key layout: K'[row][i] = K[row][pi^-1(i)] for every row of N
@@ -152,8 +171,8 @@ struct fiona_rotator {
   uint64_t *D = nullptr;               // [L][N] digits
   uint64_t *Dhat = nullptr;            // [L][L + 1][N]
   double *T = nullptr;                 // NTT intermediates, L (L + 1) vectors
-  uint64_t *U = nullptr;               // [max_rot][2][L + 1][N]
-  uint64_t *Y = nullptr;               // [max_rot][2][L][N]
+  uint64_t *U = nullptr;               // [2][n_rot][L + 1][N]
+  uint64_t *Y = nullptr;               // [2][n_rot][L][N], every limb transposed
 };
 
 namespace {
@@ -250,7 +269,10 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
     p += u_bytes;
     R->Y = (uint64_t *)p;
     const int ks_smem = (int)((L + 1) * 64 * sizeof(uint2));
+    const int g_smem = (int)(fiona::kGatherCols * ((1u << R->log_n1) + 1) * sizeof(uint64_t));
     if (!allow_smem() ||
+        hipFuncSetAttribute((const void *)fiona::gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            g_smem) != hipSuccess ||
         hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             ks_smem) != hipSuccess ||
         hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -353,15 +375,21 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
                        keys, R->U, R->limbs, N, L, n_rot);
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
 
-  // 3. the rounded division by P
-  const int rc = fiona_rescale(R->down, R->U, n_rot, R->Y, stream);
+  // 3. the rounded division by P, c0 added to the first polynomials, every
+  //    limb left transposed for the gather
+  const int rc = fiona_rescale_vectors(R->down, R->U, 2 * n_rot, R->Y, ct, n_rot, true, stream);
   if (rc != FIONA_OK) return rc;
 
-  // 4. the gather back, with c0 added to the first polynomial
-  const uint32_t gather_blocks = 8 * ((L + 7) / 8) * 2 * (N / fiona::kGatherTile);
-  for (uint32_t r = 0; r < n_rot; ++r)
-    hipLaunchKernelGGL(fiona::gather_kernel, dim3(gather_blocks), dim3(fiona::kGatherTile), 0, stream, ct,
-                       R->Y + (size_t)r * 2 * L * N, out_cts + (size_t)r * 2 * L * N, R->limbs, N, L, galois[r]);
+  // 4. the gather back to the natural frame
+  const uint32_t blocks = (N >> R->log_n1) / fiona::kGatherCols;
+  const size_t g_smem = (size_t)fiona::kGatherCols * ((1u << R->log_n1) + 1) * sizeof(uint64_t);
+  for (uint32_t r0 = 0; r0 < n_rot; r0 += fiona::kGatherMaxRot) {
+    const uint32_t nr = n_rot - r0 < fiona::kGatherMaxRot ? n_rot - r0 : fiona::kGatherMaxRot;
+    fiona::GatherArgs G{};
+    for (uint32_t r = 0; r < nr; ++r) G.g[r] = galois[r0 + r];
+    hipLaunchKernelGGL(fiona::gather_kernel, dim3(2 * nr * L * blocks), dim3(fiona::kGatherThreads), g_smem, stream,
+                       R->Y, out_cts, R->log_n1, R->log_n2, L, n_rot, r0, nr, G);
+  }
   return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
 }
 
