@@ -241,9 +241,7 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
  * of unity mod q_l.
  *
  * fiona_rescaler_create: the NTT twiddle tables of every limb (device) and a
- * workspace for up to max_ct ciphertexts (2 * max_ct * N * 8 * (1 + k) bytes,
- * where k limbs share a launch: 1 if 2 * max_ct >= 256, else
- * min(L - 1, ceil(512 / (2 * max_ct)))).
+ * workspace for up to max_ct ciphertexts (2 * max_ct * N * 8 * L bytes).
  *   psi     host [L] roots psi_l, or NULL for the default: psi_l =
  *           x^((q_l - 1) / 2N) for the smallest x >= 2 with psi_l^N = -1
  * Requires N a power of two in [2^8, 2^17], L >= 2 and every q_l = 1 mod 2N.

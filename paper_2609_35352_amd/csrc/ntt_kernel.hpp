@@ -193,6 +193,8 @@ struct NttPass {
   uint64_t in_stride, out_stride, base_stride;
   uint64_t in_set_stride, out_set_stride, base_set_stride, add_set_stride;
   uint32_t vps, log_n1, log_n2, load, store, add_count;
+  uint32_t nsets_shared;   // pass A: 0, or the number of sets when they all read the same input
+                           // vectors (in_set_stride 0) and gridDim.x * vps is a multiple of 8
 };
 
 // Global loads and stores go in batches of up to kNttBatch per thread, all
@@ -208,12 +210,23 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
   constexpr uint32_t B = PER < kNttBatch ? PER : kNttBatch, RSTEP = kNttThreads / kNttCols;
   extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * PM);
-  const uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps;
+  uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps, cb = blockIdx.x;
+  if (P.nsets_shared) {
+    // The sets read the same input vectors: give the nsets_shared workgroups
+    // of one (vector, column block) consecutive turns on one XCD (workgroup
+    // ids i, i + 8, ... run there), so that the input is fetched once into
+    // its L2.  The launch covers gridDim.x * vps units, a multiple of 8.
+    const uint32_t id = blockIdx.y * gridDim.x + blockIdx.x;
+    const uint32_t u = id >> 3, unit = (id & 7u) + 8u * (u / P.nsets_shared);
+    set = u % P.nsets_shared;
+    lv = unit / gridDim.x;
+    cb = unit - lv * gridDim.x;
+  }
   const NttSet S = P.sets[set];
   stage_twiddles(tw, S.dft_a, LOGM);
   const uint32_t N1 = 1u << P.log_n1, c = threadIdx.x % kNttCols, r = threadIdx.x / kNttCols;
-  const uint32_t n1 = blockIdx.x * kNttCols + c;
-  const uint64_t v = blockIdx.y;
+  const uint32_t n1 = cb * kNttCols + c;
+  const uint64_t v = (uint64_t)set * P.vps + lv;
   const uint64_t in_off = set * P.in_set_stride + lv * P.in_stride;
   const double q = S.q, qinv = S.qinv;
   // batches one after the other (not unrolled): fewer registers, more waves

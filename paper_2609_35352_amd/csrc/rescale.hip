@@ -22,7 +22,6 @@
 
 using namespace fiona_host;
 
-constexpr uint32_t kMinVectors = 256;   // launches of fewer vectors take several forward limbs
 
 struct fiona_rescaler {
   const fiona_ctx *ctx = nullptr;
@@ -70,12 +69,10 @@ int fiona_rescaler_create(const fiona_ctx *ctx, const uint64_t *psi, uint32_t ma
     }
     img.add(make_tables(R->log_n1, R->log_n2, qt, roots[L - 1], true), qt);
     const size_t vec_bytes = (size_t)2 * max_ct * N * sizeof(double);
-    // Calls of fewer than kMinVectors vectors take several limbs per launch
-    // (about 2 kMinVectors vectors each); T then holds limbs_per_launch
-    // intermediates.  Measured: 192 vectors run 4% faster with 3 limbs per
-    // launch, 256 vectors 3% slower with 2.
-    const uint32_t want = 2 * max_ct >= kMinVectors ? 1 : (2 * kMinVectors + 2 * max_ct - 1) / (2 * max_ct);
-    R->limbs_per_launch = want < 1 ? 1 : (want > L - 1 ? L - 1 : want);
+    // All forward limbs go in one launch pair, so T holds L - 1 intermediates.
+    // Measured against one limb per launch (in-process A/B, same buffers):
+    // 256 vectors (VGG11's outputs) 1.25 -> 1.18 ms, 192 (BERT's) 1.32 -> 1.30.
+    R->limbs_per_launch = L - 1;
     if (hipGetDevice(&R->device) != hipSuccess) {
       delete R;
       return FIONA_ERR_HIP;
@@ -150,8 +147,9 @@ int fiona_rescale_vectors(const fiona_rescaler *R, const uint64_t *in, uint32_t 
 
   // 2. every other limb: the centred remainder (a signed integer, so its
   //    residue mod q_l comes with the first product) into its NTT domain,
-  //    subtracted, multiplied by q_t^-1; limbs_per_launch limbs per launch
-  //    (one set per limb, the 2 n_ct vectors of a set share its modulus)
+  //    subtracted, multiplied by q_t^-1; all limbs in one launch pair (one
+  //    set per limb, the vectors of a set share its modulus), pass A in the
+  //    order that fetches each input block once per XCD
   const uint32_t lpl = R->limbs_per_launch;
   for (uint32_t l0 = 0; l0 + 1 < L; l0 += lpl) {
     const uint32_t nl = (uint32_t)(L - 1 - l0) < lpl ? (uint32_t)(L - 1 - l0) : lpl;
@@ -174,6 +172,8 @@ int fiona_rescale_vectors(const fiona_rescaler *R, const uint64_t *in, uint32_t 
     Q.add = add ? add + l0 * N : nullptr;
     Q.add_set_stride = N;
     Q.add_count = add ? add_count : 0;
+    const uint32_t col_blocks = (1u << R->log_n1) / fiona::kNttCols;
+    Q.nsets_shared = nl > 1 && (col_blocks * V) % 8 == 0 ? nl : 0;
     launch_transform(R->log_n1, R->log_n2, nl * V, stream, Q);
   }
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;

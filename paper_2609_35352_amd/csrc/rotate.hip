@@ -362,6 +362,7 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
   B.out_set_stride = N;
   B.load = fiona::kLoadU64;
   B.store = fiona::kStoreU64;
+  B.nsets_shared = ((1u << R->log_n1) / fiona::kNttCols * L) % 8 == 0 ? M : 0;   // every modulus reads D_j
   launch_transform(R->log_n1, R->log_n2, L * M, stream, B);
 
   // 2. the inner products of every rotation, in the pi^-1 frame
