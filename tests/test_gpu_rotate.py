@@ -167,3 +167,39 @@ def test_rotate_argument_errors():
     assert e.value.status == -5
     fiona.hoisted_rotate(rot, ct_t, [], k_t, out)   # nothing to do
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name,steps,check", [
+    ("vit768", [1, 5, 23], [0, 2]),
+    ("large4096", [1, 2, 64, 127], [0, 3]),
+])
+def test_rotate_full_size_batched_digits(name, steps, check):
+    """The full rings with L > 8 (digit batches of 16, padded for L = 10):
+    keys drawn on the device in natural order, rotations checked in full."""
+    import synth.gpu
+    dev = _dev()
+    cfg = synth.CONFIGS[name]
+    N, L = cfg.N, cfg.L
+    ps = synth.ntt_primes(N, L + 1)
+    moduli, P = ps[:L], ps[L]
+    galois = [orot.galois_element(r, N) for r in steps]
+    ctx = fiona.Ctx(N, L, moduli)
+    rot = fiona.Rotator(ctx, P, len(galois))
+    kw = rot.key_words()
+    nat_words = L * 2 * (L + 1) * N
+    nat = torch.empty(len(galois) * nat_words, dtype=torch.int64, device=dev)
+    synth.gpu.fill_rows(nat, len(galois) * L * 2 * (L + 1), moduli + [P], N, 41, synth.TAG_KEY)
+    lib_keys = torch.empty(len(galois) * kw, dtype=torch.int64, device=dev)
+    for r, g in enumerate(galois):
+        fiona.rotation_key_layout(rot, g, nat[r * nat_words:(r + 1) * nat_words], lib_keys[r * kw:(r + 1) * kw])
+    rng = np.random.default_rng(43)
+    ct = np.stack([np.stack([rng.integers(0, q, N, dtype=np.uint64) for q in moduli]) for _ in range(2)])
+    out = torch.empty(len(galois) * 2 * L * N, dtype=torch.int64, device=dev)
+    print("[rotate] full size %s N=%d L=%d steps=%s" % (name, N, L, steps), flush=True)
+    fiona.hoisted_rotate(rot, _u64(ct, dev), galois, lib_keys, out)
+    torch.cuda.synchronize()
+    got = _host(out, (len(galois), 2, L, N))
+    for r in check:
+        key = _host(nat[r * nat_words:(r + 1) * nat_words], (L, 2, L + 1, N))
+        want = orot.rotate(ct, galois[r], key, moduli, P)
+        assert np.array_equal(got[r], want), "%s rotation %d differs" % (name, r)
