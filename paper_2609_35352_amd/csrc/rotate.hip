@@ -41,20 +41,29 @@ namespace fiona {
 
 constexpr uint32_t kKsTile = 64;    // coefficients per workgroup of the inner product (one per lane)
 constexpr uint32_t kKsWaves = 8;    // wavefronts per workgroup; rotations are dealt out to them
+constexpr uint32_t kKsRoundRot = 64;   // rotations whose outputs are buffered in LDS per round (64 KiB)
+
+// LDS of the inner product: the digits, the zero row and the round's outputs.
+__host__ __device__ constexpr size_t ks_lds_bytes(uint32_t L) {
+  return (size_t)(L + 1) * 64 * sizeof(uint2) + (size_t)kKsRoundRot * 2 * 64 * sizeof(uint64_t);
+}
 
 // Step 2.  Workgroup = (modulus m, tile of 64 coefficients).  The L digits of
 // the tile are staged in LDS as radix-2^25 digit pairs; each wavefront then
 // takes rotations r = wave, wave + kKsWaves, ..., loads the 2 L key words of
 // each lane in batches of JB digits (both polynomials), and accumulates the
 // exact products (modarith.hpp), reduced once per output.  Padding terms of a
-// batch read the zero row and repeat a real key address.
+// batch read the zero row and repeat a real key address.  The outputs of up
+// to kKsRoundRot rotations wait in LDS and leave together after a barrier
+// (writes mixed one by one into the key stream cost more: 2-3% measured).
 template <uint32_t JB>
 __global__ void __launch_bounds__(kKsWaves * 64) ks_inner_kernel(const uint64_t *__restrict__ dhat,
                                                                   const uint64_t *__restrict__ keys,
                                                                   uint64_t *__restrict__ u,
                                                                   const LimbConst *__restrict__ limbs, uint32_t N,
                                                                   uint32_t L, uint32_t n_rot) {
-  extern __shared__ uint2 ks_lds[];   // [L + 1][64]: digits of Dhat[j][m] at this tile, then a zero row
+  extern __shared__ uint2 ks_lds[];   // [L + 1][64] digits of Dhat[j][m] at this tile and a zero row,
+                                      // then [kKsRoundRot][2][64] outputs of a round
   uint2 *xs = ks_lds;
   const uint32_t tiles = N / kKsTile;
   const uint32_t m = blockIdx.x / tiles, t = blockIdx.x - m * tiles;
@@ -70,30 +79,39 @@ __global__ void __launch_bounds__(kKsWaves * 64) ks_inner_kernel(const uint64_t 
   const LimbConst lc = limbs[m];
   const size_t poly = (size_t)M * N;           // words between the two polynomials of a digit
   const size_t rot_words = (size_t)L * 2 * poly;
-  for (uint32_t r = wave; r < n_rot; r += kKsWaves) {
-    const uint64_t *kr = keys + (size_t)r * rot_words + (size_t)m * N + k;
-    Acc a0, a1;
-    acc_zero(a0);
-    acc_zero(a1);
-    for (uint32_t j0 = 0; j0 < L; j0 += JB) {
-      uint64_t w0[JB], w1[JB];
+  uint64_t *obuf = (uint64_t *)(xs + M * 64);
+  for (uint32_t r0 = 0; r0 < n_rot; r0 += kKsRoundRot) {   // uniform over the workgroup
+    const uint32_t nr = n_rot - r0 < kKsRoundRot ? n_rot - r0 : kKsRoundRot;
+    for (uint32_t rr = wave; rr < nr; rr += kKsWaves) {
+      const uint64_t *kr = keys + (size_t)(r0 + rr) * rot_words + (size_t)m * N + k;
+      Acc a0, a1;
+      acc_zero(a0);
+      acc_zero(a1);
+      for (uint32_t j0 = 0; j0 < L; j0 += JB) {
+        uint64_t w0[JB], w1[JB];
 #pragma unroll
-      for (uint32_t b = 0; b < JB; ++b) {
-        const uint32_t j = j0 + b < L ? j0 + b : L - 1;
-        w0[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly);
-        w1[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly + poly);
-      }
+        for (uint32_t b = 0; b < JB; ++b) {
+          const uint32_t j = j0 + b < L ? j0 + b : L - 1;
+          w0[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly);
+          w1[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly + poly);
+        }
 #pragma unroll
-      for (uint32_t b = 0; b < JB; ++b) {
-        const uint32_t row = j0 + b < L ? j0 + b : L;
-        const uint2 x = xs[row * 64 + lane];
-        mac(a0, x.x, x.y, (uint32_t)w0[b], (uint32_t)(w0[b] >> 32));
-        mac(a1, x.x, x.y, (uint32_t)w1[b], (uint32_t)(w1[b] >> 32));
+        for (uint32_t b = 0; b < JB; ++b) {
+          const uint32_t row = j0 + b < L ? j0 + b : L;
+          const uint2 x = xs[row * 64 + lane];
+          mac(a0, x.x, x.y, (uint32_t)w0[b], (uint32_t)(w0[b] >> 32));
+          mac(a1, x.x, x.y, (uint32_t)w1[b], (uint32_t)(w1[b] >> 32));
+        }
       }
+      obuf[(2 * rr) * 64 + lane] = finish(a0, 0, lc);
+      obuf[(2 * rr + 1) * 64 + lane] = finish(a1, 0, lc);
     }
-    uint64_t *ur = u + ((size_t)r * M + m) * N + k;   // u: [2][n_rot][L + 1][N]
-    __builtin_nontemporal_store(finish(a0, 0, lc), ur);
-    __builtin_nontemporal_store(finish(a1, 0, lc), ur + (size_t)n_rot * poly);
+    __syncthreads();
+    for (uint32_t e = wave; e < 2 * nr; e += kKsWaves) {   // u: [2][n_rot][L + 1][N]
+      const uint32_t p = e & 1u, r = r0 + (e >> 1);
+      __builtin_nontemporal_store(obuf[e * 64 + lane], u + (((size_t)p * n_rot + r) * M + m) * N + k);
+    }
+    __syncthreads();   // the next round refills the buffer
   }
 }
 
@@ -268,7 +286,7 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
     R->U = (uint64_t *)p;
     p += u_bytes;
     R->Y = (uint64_t *)p;
-    const int ks_smem = (int)((L + 1) * 64 * sizeof(uint2));
+    const int ks_smem = (int)fiona::ks_lds_bytes(L);
     const int g_smem = (int)(fiona::kGatherCols * ((1u << R->log_n1) + 1) * sizeof(uint64_t));
     if (!allow_smem() ||
         hipFuncSetAttribute((const void *)fiona::gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -367,7 +385,7 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
 
   // 2. the inner products of every rotation, in the pi^-1 frame
   const dim3 ks_grid(M * (N / fiona::kKsTile));
-  const size_t ks_smem = (size_t)M * 64 * sizeof(uint2);
+  const size_t ks_smem = fiona::ks_lds_bytes(L);
   if (L <= 8)
     hipLaunchKernelGGL(fiona::ks_inner_kernel<8>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat, keys,
                        R->U, R->limbs, N, L, n_rot);

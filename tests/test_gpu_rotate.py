@@ -203,3 +203,16 @@ def test_rotate_full_size_batched_digits(name, steps, check):
         key = _host(nat[r * nat_words:(r + 1) * nat_words], (L, 2, L + 1, N))
         want = orot.rotate(ct, galois[r], key, moduli, P)
         assert np.array_equal(got[r], want), "%s rotation %d differs" % (name, r)
+
+
+def test_rotate_two_output_rounds():
+    """More rotations than one round of buffered outputs (64): 70 rotations,
+    the round edges checked against the oracle."""
+    dev = _dev()
+    N, L = 256, 2
+    steps = list(range(1, 71))
+    galois = [orot.galois_element(r, N) for r in steps]
+    moduli, P, ct, keys = _random_case(N, L, len(galois), 12)
+    got, _, _ = _run_gpu(moduli, P, ct, keys, galois, dev)
+    for r in (0, 1, 62, 63, 64, 65, 69):
+        np.testing.assert_array_equal(got[r], orot.rotate(ct, galois[r], keys[r], moduli, P))
