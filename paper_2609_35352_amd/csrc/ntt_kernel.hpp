@@ -90,8 +90,10 @@ __host__ __device__ constexpr uint32_t padded_len(uint32_t m) { return m + m / 1
 // a group is the 2^R words base + (u << s0) that these stages combine; the
 // item holds 16 >> R groups, kept in registers across the R stages.
 // Entries are |x| <= 0.57 q; every second stage and the last one end with a
-// reduction, so a product's input stays below 1.1 q and every value below
-// 1.7 q; the item leaves |x| <= q/2 behind.
+// reduction.  A product's output is below 0.5 q (1 + 2^-3); the unit-twiddle
+// butterflies of the first pass add their input unmultiplied, so a product's
+// input stays below 1.2 q, every value below 2.3 q (< 2^52, within reduce's
+// range), and the item leaves |x| <= q/2 behind.
 template <int R>
 __device__ __forceinline__ void dft_item(double *col, uint32_t logM, uint32_t s0, uint32_t item, const Tw *tw,
                                          double q, double qinv) {
@@ -111,7 +113,10 @@ __device__ __forceinline__ void dft_item(double *col, uint32_t logM, uint32_t s0
       for (uint32_t u0 = 0; u0 < S; ++u0) {
         if ((u0 & (2 * hh - 1)) >= hh) continue;
         const uint32_t pos = o + ((u0 & (hh - 1)) << s0);
-        const double a = r[u0], t = mul_tw(r[u0 + hh], tw[pos << shift], q);
+        // in the first pass (s0 = 0, so o = 0) the butterflies with pos = 0
+        // have the twiddle 1: no product (their t is at most the input bound)
+        const bool unit = s0 == 0 && (u0 & (hh - 1)) == 0;
+        const double a = r[u0], t = unit ? r[u0 + hh] : mul_tw(r[u0 + hh], tw[pos << shift], q);
         r[u0] = a + t;
         r[u0 + hh] = a - t;
       }
