@@ -286,13 +286,13 @@ int fiona_rescale(const fiona_rescaler *rescaler, const uint64_t *in_cts, uint32
  * as for the rescaler, for every modulus including P.
  *
  * fiona_rotator_create: NTT tables of q_0 .. q_{L-1} and P, and a workspace
- * for up to max_rot rotations per call (about 8 N (L (L+1) 2 + max_rot (4 L + 6))
- * bytes).
+ * for up to max_rot rotations per call (max_rot <= 256; about
+ * 8 N (2 L (L + 1) + 2 L + max_rot (4 L + 4)) bytes).
  *   special_prime  P with 2^20 < P < 2^50, P = 1 mod 2N, unequal to every q_l
  *   psi            host [L + 1] roots (the data moduli, then P) or NULL for
  *                  the defaults of fiona_rescaler_create
- * Requires N a power of two in [2^8, 2^17] and L + 1 <= FIONA_MAX_L.  Keeps a
- * reference to ctx.  Errors: FIONA_ERR_ARG, FIONA_ERR_UNSUPPORTED,
+ * Requires N a power of two in [2^8, 2^17], L + 1 <= FIONA_MAX_L and
+ * max_rot <= 256.  Keeps a reference to ctx.  Errors: FIONA_ERR_ARG, FIONA_ERR_UNSUPPORTED,
  * FIONA_ERR_NOMEM, FIONA_ERR_HIP.
  *
  * Keys.  A rotation's key holds, for digit j < L and polynomial p in {0, 1},
@@ -301,8 +301,9 @@ int fiona_rescale(const fiona_rescaler *rescaler, const uint64_t *in_cts, uint32
  * words).  In its natural order, sum_j D_j ksk[j][0] + (sum_j D_j ksk[j][1]) s
  * = P D sigma_g(s) + small for a key that switches sigma_g(s) to s.
  * fiona_hoisted_rotate reads keys in the library's layout: each row of N
- * words permuted by the rotation's slot map, written by
- * fiona_rotation_key_layout from a key in natural order (once per key).
+ * words permuted by the rotation's slot map and stored transposed (N = N1 N2
+ * as in the NTT passes), written by fiona_rotation_key_layout from a key in
+ * natural order (once per key).
  *
  * fiona_rotation_key_layout: key_out = the library layout of key (both device,
  *   fiona_rotation_key_words words, not overlapping) for Galois element

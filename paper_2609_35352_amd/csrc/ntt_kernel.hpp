@@ -160,16 +160,18 @@ __device__ __forceinline__ void stage_twiddles(Tw *dst, const Tw *__restrict__ s
 }
 
 // What a pass reads (pass A) and writes (pass B).
+// The transposed layout of an N-word vector: element i = k2 + N2 k1
+// (k2 < N2, k1 < N1, the split of the four-step transform's output) at
+// k2 N1 + k1, so that one pass-B row k2 is N1 contiguous words.
 enum NttLoad : uint32_t {
-  kLoadU64 = 0,   // residues in [0, q) as uint64
-  kLoadF64 = 1,   // signed integers as doubles, |x| < 2^49 (a centred residue of another modulus)
+  kLoadU64 = 0,    // residues in [0, q) as uint64
+  kLoadF64 = 1,    // signed integers as doubles, |x| < 2^49 (a centred residue of another modulus)
+  kLoadU64T = 2,   // residues in [0, q) as uint64, each vector in the transposed layout (no pre)
 };
 enum NttStore : uint32_t {
   kStoreU64 = 0,      // the transform, residues in [0, q) as uint64
   kStoreF64 = 1,      // the transform, centred residues as doubles
   kStoreRescale = 2,  // (base - transform) * inv mod q, in [0, q) as uint64
-  kStoreRescaleT = 3, // the same, plus add[k] for the first add_count vectors of each set, stored
-                      // transposed: element k2 + N2 k1 at k2 N1 + k1
 };
 
 // One modulus of a pass and its tables.
@@ -194,10 +196,11 @@ struct NttPass {
   void *out;             // pass B output
   const uint64_t *base;  // kStoreRescale: residues in [0, q)
   const NttSet *sets;    // device array, one entry per set
-  const uint64_t *add;   // kStoreRescaleT: residues in [0, q), set s at add + s * add_set_stride
+  const uint64_t *add;   // ntt_pass_b_rot: residues in [0, q) added to the first polynomials
   uint64_t in_stride, out_stride, base_stride;
   uint64_t in_set_stride, out_set_stride, base_set_stride, add_set_stride;
-  uint32_t vps, log_n1, log_n2, load, store, add_count;
+  uint32_t vps, log_n1, log_n2, load, store;
+  uint32_t out_transposed;  // pass B, kStoreU64 and kStoreRescale: write the transposed layout
   uint32_t nsets_shared;   // pass A: 0, or the number of sets when they all read the same input
                            // vectors (in_set_stride 0) and gridDim.x * vps is a multiple of 8
 };
@@ -234,6 +237,23 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
   const uint64_t v = (uint64_t)set * P.vps + lv;
   const uint64_t in_off = set * P.in_set_stride + lv * P.in_stride;
   const double q = S.q, qinv = S.qinv;
+  if (P.load == kLoadU64T) {   // uniform: thread t reads column cb*16 + t/16, so that each
+                               // quarter wave reads 16 consecutive words of the transposed layout
+    const uint32_t cc = threadIdx.x / kNttCols, kk = threadIdx.x % kNttCols, col = cb * kNttCols + cc;
+    const uint64_t *in = (const uint64_t *)P.in + in_off;
+    const uint32_t N2 = 1u << P.log_n2;
+#pragma unroll 1
+    for (uint32_t b0 = 0; b0 < PER; b0 += B) {
+      double x[B];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) {
+        const uint32_t n = col + N1 * (kk + (b0 + j) * kNttCols);   // element n = n1 + N1 n2
+        x[j] = reduce(to_f64(in[(size_t)(n & (N2 - 1)) * N1 + (n >> P.log_n2)]), q, qinv);
+      }
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) xs[cc * PM + pidx(bit_reverse(kk + (b0 + j) * kNttCols, LOGM))] = x[j];
+    }
+  } else {
   // batches one after the other (not unrolled): fewer registers, more waves
 #pragma unroll 1
   for (uint32_t b0 = 0; b0 < PER; b0 += B) {
@@ -259,6 +279,7 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
     }
 #pragma unroll
     for (uint32_t j = 0; j < B; ++j) xs[c * PM + pidx(bit_reverse(r + (b0 + j) * RSTEP, LOGM))] = x[j];
+  }
   }
   lds_dft<LOGM>(xs, tw, q, qinv);
   double *tmp = P.tmp + v * ((uint64_t)N1 * M) + n1;
@@ -303,10 +324,9 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
   }
   lds_dft<LOGM>(xs, tw, q, qinv);
   const uint32_t c = threadIdx.x % kNttCols, r = threadIdx.x / kNttCols, k2 = r0 + c;
-  const bool transposed = P.store == kStoreRescaleT;
-  const bool rescale = P.store == kStoreRescale || transposed;
+  const bool transposed = P.out_transposed != 0 && P.store != kStoreF64;
+  const bool rescale = P.store == kStoreRescale;
   const uint64_t *base = rescale ? P.base + set * P.base_set_stride + lv * P.base_stride + k2 : nullptr;
-  const uint64_t *add = transposed && lv < P.add_count ? P.add + set * P.add_set_stride + k2 : nullptr;
 #pragma unroll
   for (uint32_t b0 = 0; b0 < PER; b0 += B) {
     double y[B];
@@ -334,16 +354,6 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
     }
 #pragma unroll
     for (uint32_t j = 0; j < B; ++j) y[j] = canonical(y[j], q, qinv);
-    if (add) {
-      uint64_t av[B];
-#pragma unroll
-      for (uint32_t j = 0; j < B; ++j) av[j] = add[(size_t)N2 * (r + (b0 + j) * RSTEP)];
-#pragma unroll
-      for (uint32_t j = 0; j < B; ++j) {
-        const double z = y[j] + to_f64(av[j]);
-        y[j] = z >= q ? z - q : z;
-      }
-    }
     if (transposed) {
 #pragma unroll
       for (uint32_t j = 0; j < B; ++j) xs[c * PM + pidx(r + (b0 + j) * RSTEP)] = y[j];

@@ -18,7 +18,6 @@
 #include "fiona.h"
 #include "fiona_ctx.hpp"
 #include "ntt_host.hpp"
-#include "rescale_internal.hpp"
 
 using namespace fiona_host;
 
@@ -119,16 +118,7 @@ int fiona_rescale(const fiona_rescaler *R, const uint64_t *in_cts, uint32_t n_ct
   if (a0 < b0 + out_bytes && b0 < a0 + in_bytes) return FIONA_ERR_ALIAS;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != R->device) return FIONA_ERR_ARG;
-  return fiona_rescale_vectors(R, in_cts, 2 * n_ct, out_cts, nullptr, 0, false, stream);
-}
-
-}  // extern "C"
-
-int fiona_rescale_vectors(const fiona_rescaler *R, const uint64_t *in, uint32_t V, uint64_t *out,
-                          const uint64_t *add, uint32_t add_count, bool transposed, hipStream_t stream) {
-  const size_t N = R->N, L = R->L;
-  const uint64_t *in_cts = in;
-  uint64_t *out_cts = out;
+  const uint32_t V = 2 * n_ct;
 
   // 1. the last limb back to its coefficients, kept as centred residues mod q_t
   NttPass P{};
@@ -168,10 +158,7 @@ int fiona_rescale_vectors(const fiona_rescaler *R, const uint64_t *in, uint32_t 
     Q.base_stride = L * N;
     Q.base_set_stride = N;
     Q.load = fiona::kLoadF64;
-    Q.store = transposed ? fiona::kStoreRescaleT : fiona::kStoreRescale;
-    Q.add = add ? add + l0 * N : nullptr;
-    Q.add_set_stride = N;
-    Q.add_count = add ? add_count : 0;
+    Q.store = fiona::kStoreRescale;
     const uint32_t col_blocks = (1u << R->log_n1) / fiona::kNttCols;
     Q.nsets_shared = nl > 1 && (col_blocks * V) % 8 == 0 ? nl : 0;
     launch_transform(R->log_n1, R->log_n2, nl * V, stream, Q);
@@ -179,5 +166,7 @@ int fiona_rescale_vectors(const fiona_rescaler *R, const uint64_t *in, uint32_t 
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   return FIONA_OK;
 }
+
+}  // extern "C"
 
 

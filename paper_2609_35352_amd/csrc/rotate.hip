@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <algorithm>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -33,7 +34,6 @@
 #include "fiona_ctx.hpp"
 #include "modarith.hpp"
 #include "ntt_host.hpp"
-#include "rescale_internal.hpp"
 
 using namespace fiona_host;
 
@@ -115,87 +115,179 @@ __global__ void __launch_bounds__(kKsWaves * 64) ks_inner_kernel(const uint64_t 
   }
 }
 
-// Step 4.  The division by P leaves every limb of v' transposed: element
-// k = k2 + N2 k1 at k2 N1 + k1 (N = N1 N2, the four-step split).  With
-// d = d_lo + N2 d_hi and A = (g d_lo + c) mod N, pi(d) = k2 + N2 k1 with
-// k2 = A mod N2 and k1 = (A / N2 + g d_hi) mod N1: the 16 destinations
-// d_lo .. d_lo + 15 of every d_hi read the 16 source rows k2 = A mod N2.  A
-// workgroup (vector, limb, 16 consecutive d_lo) loads those rows whole
-// (contiguous N1 words each) into LDS, then stores its destinations as runs
-// of 16 words.  The Galois elements of up to kGatherMaxRot rotations ride in
-// the arguments.
-constexpr uint32_t kGatherThreads = 256;
-constexpr uint32_t kGatherCols = 16;
-constexpr uint32_t kGatherMaxRot = 256;
+// Steps 3-4 fused: the forward pass B of the division by P that also applies
+// the automorphism.  With d = d_lo + N2 d_hi and A = (g d_lo + c) mod N
+// (c = (g - 1) / 2), pi(d) = k2 + N2 k1 where k2 = A mod N2 depends on d_lo
+// only and k1 = (A / N2 + g d_hi) mod N1.  A workgroup takes 16 consecutive
+// destination columns d_lo, transforms the 16 intermediate rows k2 they read
+// (contiguous rows of N1 words), finishes the division there (u' and c0 are
+// in the transposed layout, so row k2 is contiguous too), and then stores
+// each destination row d_hi as a run of 16 words, picking k1 in LDS.
+// Vectors: set = data limb l, vector lv = p n_rot + r in the set.
+constexpr uint32_t kRotMax = 256;   // rotations per call (their Galois elements ride in the arguments)
 
-struct GatherArgs {
-  uint32_t g[kGatherMaxRot];
+struct RotArgs {
+  uint32_t g[kRotMax];
+  uint32_t n_rot, L;
 };
 
-__global__ void __launch_bounds__(kGatherThreads) gather_kernel(const uint64_t *__restrict__ vt,
-                                                                uint64_t *__restrict__ out, uint32_t log_n1,
-                                                                uint32_t log_n2, uint32_t L, uint32_t n_rot,
-                                                                uint32_t r0, uint32_t nr, const GatherArgs G) {
-  extern __shared__ uint64_t gather_lds[];   // [kGatherCols][N1 + 1]
-  const uint32_t N1 = 1u << log_n1, N2 = 1u << log_n2, N = N1 * N2, PM = N1 + 1;
-  const uint32_t blocks = N2 / kGatherCols;
-  const uint32_t blk = blockIdx.x % blocks, rest = blockIdx.x / blocks;
-  const uint32_t limb = rest % L, lv = rest / L;   // lv = p nr + local rotation
-  const uint32_t p = lv / nr, rl = lv - p * nr, r = r0 + rl;
-  const uint32_t g = G.g[rl], c = (g - 1) / 2;
-  const uint32_t o0 = blk * kGatherCols;
-  const uint64_t *src = vt + ((size_t)(p * n_rot + r) * L + limb) * N;
-  for (uint32_t w = threadIdx.x; w < kGatherCols * N1; w += kGatherThreads) {
-    const uint32_t col = w >> log_n1, row = w & (N1 - 1);
-    const uint32_t k2 = (g * (o0 + col) + c) & (N2 - 1);   // A mod N2 (N2 divides 2^32)
-    gather_lds[col * PM + row] = src[(size_t)k2 * N1 + row];
+template <uint32_t LOGM>
+__global__ void __launch_bounds__(kNttThreads) ntt_pass_b_rot(const NttPass P, const RotArgs R) {
+  constexpr uint32_t M = 1u << LOGM, PM = padded_len(M), PER = kNttCols * M / kNttThreads;
+  constexpr uint32_t B = PER < kNttBatch ? PER : kNttBatch;
+  extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
+  Tw *tw = (Tw *)(xs + kNttCols * PM);
+  const uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps;
+  const uint32_t p = lv / R.n_rot, r = lv - p * R.n_rot;
+  const NttSet S = P.sets[set];
+  stage_twiddles(tw, S.dft_b, LOGM);
+  const uint32_t log_n2 = P.log_n2, N2 = 1u << log_n2, N = M << log_n2;   // M = N1
+  const uint32_t g = R.g[r], cg = (g - 1) / 2, o0 = blockIdx.x * kNttCols;
+  const double q = S.q, qinv = S.qinv;
+  const double *tmp = P.tmp + (uint64_t)blockIdx.y * N;
+#pragma unroll
+  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
+    double x[B];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) {
+      const uint32_t idx = threadIdx.x + (b0 + j) * kNttThreads;
+      const uint32_t k2 = (g * (o0 + (idx >> LOGM)) + cg) & (N2 - 1);
+      x[j] = tmp[(size_t)k2 * M + (idx & (M - 1))];
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) {
+      const uint32_t idx = threadIdx.x + (b0 + j) * kNttThreads;
+      xs[(idx >> LOGM) * PM + pidx(bit_reverse(idx & (M - 1), LOGM))] = x[j];
+    }
+  }
+  lds_dft<LOGM>(xs, tw, q, qinv);
+  // row cc of the workgroup (k2 of destination column o0 + cc), k1 = kk + 16 j:
+  // (u' - transform) * P^-1, plus c0 for the first polynomial, back in place
+  const uint32_t cc = threadIdx.x / kNttCols, kk = threadIdx.x % kNttCols;
+  const uint32_t k2c = (g * (o0 + cc) + cg) & (N2 - 1);
+  const uint64_t *base = P.base + set * P.base_set_stride + lv * P.base_stride + (size_t)k2c * M;
+  const uint64_t *add = p == 0 ? P.add + set * P.add_set_stride + (size_t)k2c * M : nullptr;
+#pragma unroll 1
+  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
+    double y[B];
+    uint64_t bv[B];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) bv[j] = base[kk + (b0 + j) * kNttCols];
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) {
+      y[j] = xs[cc * PM + pidx(kk + (b0 + j) * kNttCols)];
+      y[j] = canonical(mul_tw(to_f64(bv[j]) - y[j], S.inv, q), q, qinv);
+    }
+    if (add) {
+      uint64_t av[B];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) av[j] = add[kk + (b0 + j) * kNttCols];
+#pragma unroll
+      for (uint32_t j = 0; j < B; ++j) {
+        const double z = y[j] + to_f64(av[j]);
+        y[j] = z >= q ? z - q : z;
+      }
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < B; ++j) xs[cc * PM + pidx(kk + (b0 + j) * kNttCols)] = y[j];
   }
   __syncthreads();
-  const uint32_t col = threadIdx.x % kGatherCols;
-  const uint32_t A = (g * (o0 + col) + c) & (N - 1);
-  const uint32_t hi = A >> log_n2;
-  uint64_t *dst = out + ((size_t)(r * 2 + p) * L + limb) * N + o0 + col;
-  for (uint32_t d_hi = threadIdx.x / kGatherCols; d_hi < N1; d_hi += kGatherThreads / kGatherCols) {
-    const uint32_t k1 = (hi + g * d_hi) & (N1 - 1);
-    dst[(size_t)d_hi * N2] = gather_lds[col * PM + k1];
+  // destination column o0 + c, rows d_hi = rr + 16 j: runs of 16 words
+  const uint32_t c = threadIdx.x % kNttCols, rr = threadIdx.x / kNttCols;
+  const uint32_t hi = ((g * (o0 + c) + cg) & (N - 1)) >> log_n2;
+  uint64_t *out = (uint64_t *)P.out + ((size_t)(r * 2 + p) * R.L + set) * N + o0 + c;
+#pragma unroll
+  for (uint32_t j = 0; j < PER; ++j) {
+    const uint32_t d_hi = rr + j * kNttCols;
+    const uint32_t k1 = (hi + g * d_hi) & (M - 1);
+    out[(size_t)d_hi * N2] = to_u64(xs[c * PM + pidx(k1)]);
   }
 }
 
-// The library's key layout: K'[row][i] = K[row][pi^-1(i)] for every row of N
-// words, pi^-1(i) = (i - (g - 1) / 2) g^-1 mod N.
+// c0 of the input ciphertext in the transposed layout (L limbs), for the
+// fused division: out[l][k2 N1 + k1] = c0[l][k2 + N2 k1].
+__global__ void __launch_bounds__(256) transpose_kernel(const uint64_t *__restrict__ in, uint64_t *__restrict__ out,
+                                                        uint32_t log_n1, uint32_t log_n2) {
+  const uint32_t N = 1u << (log_n1 + log_n2);
+  const uint32_t a = blockIdx.x * 256 + threadIdx.x;   // destination index
+  const size_t limb = (size_t)blockIdx.y * N;
+  if (a >= N) return;
+  const uint32_t k2 = a >> log_n1, k1 = a & ((1u << log_n1) - 1);
+  out[limb + a] = in[limb + k2 + ((size_t)k1 << log_n2)];
+}
+
+// The library's key layout: every row of N words permuted by pi^-1 and stored
+// transposed, K'[row][k2 N1 + k1] = K[row][pi^-1(k2 + N2 k1)], with
+// pi^-1(i) = (i - (g - 1) / 2) g^-1 mod N.
 __global__ void __launch_bounds__(256) key_layout_kernel(const uint64_t *__restrict__ key,
-                                                         uint64_t *__restrict__ out, uint32_t N, uint32_t rows,
-                                                         uint32_t g, uint32_t ginv) {
+                                                         uint64_t *__restrict__ out, uint32_t log_n1,
+                                                         uint32_t log_n2, uint32_t rows, uint32_t g, uint32_t ginv) {
+  const uint32_t N = 1u << (log_n1 + log_n2);
   const uint32_t row = blockIdx.y;
-  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-  if (row >= rows || i >= N) return;
+  const uint32_t a = blockIdx.x * 256 + threadIdx.x;
+  if (row >= rows || a >= N) return;
+  const uint32_t i = (a >> log_n1) + ((a & ((1u << log_n1) - 1)) << log_n2);
   const uint32_t src = ((i - (g - 1) / 2) * ginv) & (N - 1);
-  out[(size_t)row * N + i] = key[(size_t)row * N + src];
+  out[(size_t)row * N + a] = key[(size_t)row * N + src];
 }
 
 }  // namespace fiona
 
 struct fiona_rotator {
   const fiona_ctx *ctx = nullptr;
-  fiona_ctx *ext = nullptr;            // q_0 .. q_{L-1}, P
-  fiona_rescaler *down = nullptr;      // the division by P: a rescale of the extended chain
+  fiona_ctx *ext = nullptr;            // q_0 .. q_{L-1}, P (their multiply-add constants)
   uint32_t N = 0, L = 0, log_n1 = 0, log_n2 = 0, max_rot = 0;
   uint64_t P = 0;
   int device = -1;
   void *dev = nullptr;
   const NttSet *inv_sets = nullptr;    // [L] inverse transforms of q_0 .. q_{L-1}
   const NttSet *fwd_sets = nullptr;    // [L + 1] forward transforms of q_0 .. q_{L-1}, P
+  const NttSet *down_sets = nullptr;   // [L] forward transforms of q_0 .. q_{L-1}, inv = P^-1 mod q_l
+  const NttSet *p_inv_set = nullptr;   // [1] inverse transform of P
   const fiona::LimbConst *limbs = nullptr;   // [L + 1] on the device
   uint64_t *D = nullptr;               // [L][N] digits
-  uint64_t *Dhat = nullptr;            // [L][L + 1][N]
-  double *T = nullptr;                 // NTT intermediates, L (L + 1) vectors
-  uint64_t *U = nullptr;               // [2][n_rot][L + 1][N]
-  uint64_t *Y = nullptr;               // [2][n_rot][L][N], every limb transposed
+  uint64_t *Dhat = nullptr;            // [L][L + 1][N], transposed layout
+  uint64_t *c0t = nullptr;             // [L][N] c0 of the call, transposed layout
+  double *T = nullptr;                 // NTT intermediates: max(L (L + 1), 2 L max_rot) vectors
+  double *W = nullptr;                 // [2 max_rot][N] centred coefficients of u'_P
+  uint64_t *U = nullptr;               // [2][n_rot][L + 1][N], transposed layout
 };
 
 namespace {
 
 size_t round256(size_t x) { return (x + 255) / 256 * 256; }
+
+template <uint32_t LOG>
+void launch_rot_b(dim3 grid, size_t smem, hipStream_t stream, const NttPass &P, const fiona::RotArgs &G) {
+  hipLaunchKernelGGL(fiona::ntt_pass_b_rot<LOG>, grid, dim3(fiona::kNttThreads), smem, stream, P, G);
+}
+
+// The fused pass B over V vectors: grid (N2 / 16 destination blocks, V).
+void launch_rot_pass_b(uint32_t log_n1, uint32_t log_n2, uint32_t V, hipStream_t stream, const NttPass &P,
+                       const fiona::RotArgs &G) {
+  const dim3 grid((1u << log_n2) / fiona::kNttCols, V);
+  const size_t smem = fiona::kNttCols * fiona::padded_len(1u << log_n1) * sizeof(double) +
+                      (1u << log_n1) / 2 * sizeof(Tw);
+  switch (log_n1) {
+    case 4: launch_rot_b<4>(grid, smem, stream, P, G); break;
+    case 5: launch_rot_b<5>(grid, smem, stream, P, G); break;
+    case 6: launch_rot_b<6>(grid, smem, stream, P, G); break;
+    case 7: launch_rot_b<7>(grid, smem, stream, P, G); break;
+    case 8: launch_rot_b<8>(grid, smem, stream, P, G); break;
+    default: launch_rot_b<9>(grid, smem, stream, P, G); break;
+  }
+}
+
+template <uint32_t LOG>
+bool allow_rot_one(int bytes) {
+  return hipFuncSetAttribute((const void *)fiona::ntt_pass_b_rot<LOG>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             bytes) == hipSuccess;
+}
+
+bool allow_rot_smem(int bytes) {
+  return allow_rot_one<4>(bytes) && allow_rot_one<5>(bytes) && allow_rot_one<6>(bytes) &&
+         allow_rot_one<7>(bytes) && allow_rot_one<8>(bytes) && allow_rot_one<9>(bytes);
+}
 
 bool overlap(const void *a, size_t na, const void *b, size_t nb) {
   const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
@@ -215,7 +307,7 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
   uint32_t logN = 0;
   while ((1u << logN) < N) ++logN;
   if ((1u << logN) != N || logN < 8 || logN > 17 || L < 1 || L + 1 > FIONA_MAX_L) return FIONA_ERR_UNSUPPORTED;
-  if ((size_t)L * (L + 1) > 65535 || 2ull * max_rot > 65535) return FIONA_ERR_UNSUPPORTED;
+  if ((size_t)L * (L + 1) > 65535 || max_rot > fiona::kRotMax) return FIONA_ERR_UNSUPPORTED;
   const uint64_t P = special_prime;
   if (P <= (1ull << FIONA_SCALE_BITS) || P >= (1ull << FIONA_MODULUS_BITS) || (P - 1) % (2ull * N) != 0)
     return FIONA_ERR_UNSUPPORTED;
@@ -240,7 +332,6 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
   R->log_n2 = logN / 2;
   R->max_rot = max_rot;
   int rc = fiona_ctx_create(N, L + 1, mods.data(), &R->ext);
-  if (rc == FIONA_OK) rc = fiona_rescaler_create(R->ext, roots.data(), max_rot, &R->down);
   if (rc != FIONA_OK) {
     fiona_rotator_destroy(R);
     return rc;
@@ -249,18 +340,25 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
     TableImage img;
     for (uint32_t j = 0; j < L; ++j) img.add(make_tables(R->log_n1, R->log_n2, mods[j], roots[j], true), mods[j]);
     for (uint32_t i = 0; i <= L; ++i) img.add(make_tables(R->log_n1, R->log_n2, mods[i], roots[i], false), mods[i]);
+    for (uint32_t l = 0; l < L; ++l)
+      img.add(make_tables(R->log_n1, R->log_n2, mods[l], roots[l], false), mods[l],
+              make_tw(powmod_h(P % mods[l], mods[l] - 2, mods[l]), mods[l]));
+    img.add(make_tables(R->log_n1, R->log_n2, P, roots[L], true), P);
     const size_t img_bytes = img.bytes();
     const size_t limb_bytes = round256((L + 1) * sizeof(fiona::LimbConst));
-    const size_t d_bytes = round256((size_t)L * N * 8);
-    const size_t dhat_bytes = round256((size_t)L * (L + 1) * N * 8);
-    const size_t t_bytes = round256((size_t)L * (L + 1) * N * 8);
-    const size_t u_bytes = round256((size_t)max_rot * 2 * (L + 1) * N * 8);
-    const size_t y_bytes = round256((size_t)max_rot * 2 * L * N * 8);
+    const size_t vec = (size_t)N * 8;
+    const size_t d_bytes = round256(L * vec);
+    const size_t dhat_bytes = round256((size_t)L * (L + 1) * vec);
+    const size_t c0_bytes = round256(L * vec);
+    const size_t t_vectors = std::max((size_t)L * (L + 1), (size_t)2 * L * max_rot);
+    const size_t t_bytes = round256(t_vectors * vec);
+    const size_t w_bytes = round256((size_t)2 * max_rot * vec);
+    const size_t u_bytes = round256((size_t)max_rot * 2 * (L + 1) * vec);
     if (hipGetDevice(&R->device) != hipSuccess) {
       fiona_rotator_destroy(R);
       return FIONA_ERR_HIP;
     }
-    const size_t total = img_bytes + limb_bytes + d_bytes + dhat_bytes + t_bytes + u_bytes + y_bytes;
+    const size_t total = img_bytes + limb_bytes + d_bytes + dhat_bytes + c0_bytes + t_bytes + w_bytes + u_bytes;
     if (hipMalloc(&R->dev, total) != hipSuccess) {
       R->dev = nullptr;
       fiona_rotator_destroy(R);
@@ -275,22 +373,28 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
     }
     R->inv_sets = sets;
     R->fwd_sets = sets + L;
+    R->down_sets = sets + 2 * L + 1;
+    R->p_inv_set = sets + 3 * L + 1;
     R->limbs = (const fiona::LimbConst *)p;
     p += limb_bytes;
     R->D = (uint64_t *)p;
     p += d_bytes;
     R->Dhat = (uint64_t *)p;
     p += dhat_bytes;
+    R->c0t = (uint64_t *)p;
+    p += c0_bytes;
     R->T = (double *)p;
     p += t_bytes;
+    R->W = (double *)p;
+    p += w_bytes;
     R->U = (uint64_t *)p;
-    p += u_bytes;
-    R->Y = (uint64_t *)p;
     const int ks_smem = (int)fiona::ks_lds_bytes(L);
-    const int g_smem = (int)(fiona::kGatherCols * ((1u << R->log_n1) + 1) * sizeof(uint64_t));
+    const int nt_smem = (int)(fiona::kNttCols * fiona::padded_len(fiona::kNttMaxSide) * sizeof(double) +
+                              fiona::kNttMaxSide / 2 * sizeof(Tw));
     if (!allow_smem() ||
-        hipFuncSetAttribute((const void *)fiona::gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            g_smem) != hipSuccess ||
+        hipFuncSetAttribute((const void *)fiona::ntt_pass_b_rot<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            nt_smem) != hipSuccess ||
+        !allow_rot_smem(nt_smem) ||
         hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             ks_smem) != hipSuccess ||
         hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -309,7 +413,6 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
 void fiona_rotator_destroy(fiona_rotator *R) {
   if (!R) return;
   if (R->dev) (void)hipFree(R->dev);
-  fiona_rescaler_destroy(R->down);
   fiona_ctx_destroy(R->ext);
   delete R;
 }
@@ -331,8 +434,8 @@ int fiona_rotation_key_layout(const fiona_rotator *R, uint32_t galois, const uin
   uint32_t ginv = 1;   // g^-1 mod N by Newton's iteration (g odd, N a power of two)
   for (int i = 0; i < 5; ++i) ginv *= 2u - galois * ginv;
   const uint32_t rows = R->L * 2 * (R->L + 1);
-  hipLaunchKernelGGL(fiona::key_layout_kernel, dim3(N / 256, rows), dim3(256), 0, stream, key, key_out, N, rows,
-                     galois, ginv & (N - 1));
+  hipLaunchKernelGGL(fiona::key_layout_kernel, dim3(N / 256, rows), dim3(256), 0, stream, key, key_out, R->log_n1,
+                     R->log_n2, rows, galois, ginv & (N - 1));
   return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
 }
 
@@ -354,6 +457,7 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
   const uint32_t M = L + 1;
 
   // 1. digits of c1, once: D_j = INTT_{q_j}(c1_j), then Dhat[j][m] = NTT_m(D_j)
+  //    (transposed layout); c0 transposed for step 3
   NttPass A{};
   A.sets = R->inv_sets;
   A.vps = 1;
@@ -380,10 +484,13 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
   B.out_set_stride = N;
   B.load = fiona::kLoadU64;
   B.store = fiona::kStoreU64;
+  B.out_transposed = 1;
   B.nsets_shared = ((1u << R->log_n1) / fiona::kNttCols * L) % 8 == 0 ? M : 0;   // every modulus reads D_j
   launch_transform(R->log_n1, R->log_n2, L * M, stream, B);
+  hipLaunchKernelGGL(fiona::transpose_kernel, dim3((N + 255) / 256, L), dim3(256), 0, stream, ct, R->c0t, R->log_n1,
+                     R->log_n2);
 
-  // 2. the inner products of every rotation, in the pi^-1 frame
+  // 2. the inner products of every rotation (transposed layout, pi^-1 frame)
   const dim3 ks_grid(M * (N / fiona::kKsTile));
   const size_t ks_smem = fiona::ks_lds_bytes(L);
   if (L <= 8)
@@ -392,23 +499,47 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
   else
     hipLaunchKernelGGL(fiona::ks_inner_kernel<16>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat,
                        keys, R->U, R->limbs, N, L, n_rot);
-  if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
 
-  // 3. the rounded division by P, c0 added to the first polynomials, every
-  //    limb left transposed for the gather
-  const int rc = fiona_rescale_vectors(R->down, R->U, 2 * n_rot, R->Y, ct, n_rot, true, stream);
-  if (rc != FIONA_OK) return rc;
-
-  // 4. the gather back to the natural frame
-  const uint32_t blocks = (N >> R->log_n1) / fiona::kGatherCols;
-  const size_t g_smem = (size_t)fiona::kGatherCols * ((1u << R->log_n1) + 1) * sizeof(uint64_t);
-  for (uint32_t r0 = 0; r0 < n_rot; r0 += fiona::kGatherMaxRot) {
-    const uint32_t nr = n_rot - r0 < fiona::kGatherMaxRot ? n_rot - r0 : fiona::kGatherMaxRot;
-    fiona::GatherArgs G{};
-    for (uint32_t r = 0; r < nr; ++r) G.g[r] = galois[r0 + r];
-    hipLaunchKernelGGL(fiona::gather_kernel, dim3(2 * nr * L * blocks), dim3(fiona::kGatherThreads), g_smem, stream,
-                       R->Y, out_cts, R->log_n1, R->log_n2, L, n_rot, r0, nr, G);
-  }
+  // 3. the division by P: u'_P back to centred coefficients (W), then per
+  //    data limb its transform, the subtraction from u', the product with
+  //    P^-1, c0 for the first polynomials and the automorphism, written to out
+  const uint32_t V = 2 * n_rot;
+  NttPass C{};
+  C.sets = R->p_inv_set;
+  C.vps = V;
+  C.log_n1 = R->log_n1;
+  C.log_n2 = R->log_n2;
+  C.in = R->U + (size_t)L * N;
+  C.in_stride = (size_t)M * N;
+  C.tmp = R->T;
+  C.out = R->W;
+  C.out_stride = N;
+  C.load = fiona::kLoadU64T;
+  C.store = fiona::kStoreF64;
+  launch_transform(R->log_n1, R->log_n2, V, stream, C);
+  NttPass Q{};
+  Q.sets = R->down_sets;
+  Q.vps = V;
+  Q.log_n1 = R->log_n1;
+  Q.log_n2 = R->log_n2;
+  Q.in = R->W;
+  Q.in_stride = N;
+  Q.tmp = R->T;
+  Q.out = out_cts;
+  Q.base = R->U;
+  Q.base_stride = (size_t)M * N;
+  Q.base_set_stride = N;
+  Q.add = R->c0t;
+  Q.add_set_stride = N;
+  Q.load = fiona::kLoadF64;
+  const uint32_t col_blocks = (1u << R->log_n1) / fiona::kNttCols;
+  Q.nsets_shared = L > 1 && (col_blocks * V) % 8 == 0 ? L : 0;
+  launch_pass(true, R->log_n2, R->log_n1, L * V, stream, Q);
+  fiona::RotArgs G{};
+  for (uint32_t r = 0; r < n_rot; ++r) G.g[r] = galois[r];
+  G.n_rot = n_rot;
+  G.L = L;
+  launch_rot_pass_b(R->log_n1, R->log_n2, L * V, stream, Q, G);
   return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
 }
 

@@ -304,7 +304,7 @@ def test_rotator_validation():
     ps = synth.ntt_primes(N, L + 1)
     ctx = fiona.Ctx(N, L, ps[:L])
     for P, max_rot, status in [(ps[L] + 2, 1, -3), (ps[0], 1, -3), (ps[L], 0, -1), (1 << 50, 1, -3),
-                               (3, 1, -3)]:
+                               (3, 1, -3), (ps[L], 257, -3)]:
         with pytest.raises(fiona.FionaError) as e:
             fiona.Rotator(ctx, P, max_rot)
         assert e.value.status == status
