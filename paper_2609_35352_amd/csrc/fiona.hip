@@ -661,15 +661,13 @@ int upload_plan(fiona_plan *P) {
     return FIONA_ERR_HIP;
   }
   if (hipMemcpy(P->dev, host.data(), total, hipMemcpyHostToDevice) != hipSuccess) return FIONA_ERR_HIP;
-  static bool attr_set = false;
-  if (!attr_set) {
-    if (hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<8>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes) != hipSuccess ||
-        hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<16>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes) != hipSuccess)
-      return FIONA_ERR_HIP;
-    attr_set = true;
-  }
+  // the kernels' LDS limit, set on the current device with every plan (cheap,
+  // and correct whatever device the plan lives on)
+  if (hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)kLdsBytes) != hipSuccess ||
+      hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)kLdsBytes) != hipSuccess)
+    return FIONA_ERR_HIP;
   unsigned char *base = (unsigned char *)P->dev;
   P->d_limbs = (const LimbConst *)(base + o_limbs);
   P->d_items = (const uint4 *)(base + o_items);
