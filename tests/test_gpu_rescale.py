@@ -50,7 +50,7 @@ def _gpu_rescale(cts, moduli, dev, max_ct=None):
 
 
 @pytest.mark.parametrize("N,L,n_ct,seed", [(256, 2, 2, 1), (1 << 12, 3, 3, 2), (1 << 13, 5, 2, 3),
-                                           (1 << 11, 4, 1, 4)])
+                                           (1 << 11, 4, 1, 4), (1 << 17, 2, 1, 5)])
 def test_rescale_matches_oracle(dev, N, L, n_ct, seed):
     _say("[rescale] N=%d L=%d n_ct=%d seed=%d" % (N, L, n_ct, seed))
     moduli = synth.ntt_primes(N, L)

@@ -64,6 +64,7 @@ def _run_gpu(moduli, P, ct, keys, galois, dev, psi=None):
     (1024, 3, [1, 5, -1], 2),
     (4096, 4, [1, 2, 17, 1000], 3),
     (2048, 10, [7], 4),
+    (1 << 17, 2, [1, 30000], 5),   # the largest ring: DFT sides 512 x 256
 ])
 def test_rotate_matches_oracle(N, L, steps, seed):
     dev = _dev()
