@@ -241,10 +241,13 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
  * of unity mod q_l.
  *
  * fiona_rescaler_create: the NTT twiddle tables of every limb (device) and a
- * workspace for up to max_ct ciphertexts (2 * max_ct * N * 8 * L bytes).
+ * workspace for up to max_ct ciphertexts (2 * max_ct * N * 8 * (1 + k) bytes,
+ * k = L - 1 limbs per launch, fewer when that would pass 8 GiB or 65535
+ * vectors).
  *   psi     host [L] roots psi_l, or NULL for the default: psi_l =
  *           x^((q_l - 1) / 2N) for the smallest x >= 2 with psi_l^N = -1
- * Requires N a power of two in [2^8, 2^17], L >= 2 and every q_l = 1 mod 2N.
+ * Requires N a power of two in [2^8, 2^17], L >= 2, every q_l = 1 mod 2N and
+ * max_ct <= 32767.
  * The rescaler keeps a reference to ctx (which must outlive it).  Errors:
  * FIONA_ERR_ARG, FIONA_ERR_UNSUPPORTED (N, L, a modulus or a root),
  * FIONA_ERR_NOMEM, FIONA_ERR_HIP.

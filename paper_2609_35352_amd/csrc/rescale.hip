@@ -21,6 +21,8 @@
 
 using namespace fiona_host;
 
+constexpr size_t kMaxTmpBytes = (size_t)8 << 30;   // cap on the intermediates of one launch pair
+
 
 struct fiona_rescaler {
   const fiona_ctx *ctx = nullptr;
@@ -39,6 +41,7 @@ int fiona_rescaler_create(const fiona_ctx *ctx, const uint64_t *psi, uint32_t ma
   if (!out) return FIONA_ERR_ARG;
   *out = nullptr;
   if (!ctx || max_ct == 0) return FIONA_ERR_ARG;
+  if (2ull * max_ct > 65535) return FIONA_ERR_UNSUPPORTED;   // a launch holds at most 65535 vectors
   const uint32_t N = ctx->N, L = ctx->L;
   uint32_t logN = 0;
   while ((1u << logN) < N) ++logN;
@@ -71,7 +74,14 @@ int fiona_rescaler_create(const fiona_ctx *ctx, const uint64_t *psi, uint32_t ma
     // All forward limbs go in one launch pair, so T holds L - 1 intermediates.
     // Measured against one limb per launch (in-process A/B, same buffers):
     // 256 vectors (VGG11's outputs) 1.25 -> 1.18 ms, 192 (BERT's) 1.32 -> 1.30.
-    R->limbs_per_launch = L - 1;
+    // Very large max_ct takes fewer limbs per launch, so that T stays within
+    // kMaxTmpBytes (and every launch within the grid's 65535 vectors).
+    const size_t fit = kMaxTmpBytes / vec_bytes;
+    const size_t fit_grid = 65535 / (2 * (size_t)max_ct);
+    size_t lpl = L - 1;
+    if (lpl > fit) lpl = fit;
+    if (lpl > fit_grid) lpl = fit_grid;
+    R->limbs_per_launch = lpl < 1 ? 1 : (uint32_t)lpl;
     if (hipGetDevice(&R->device) != hipSuccess) {
       delete R;
       return FIONA_ERR_HIP;

@@ -313,3 +313,12 @@ def test_rotator_validation():
         fiona.Rotator(small, synth.ntt_primes(128, L + 1)[L], 1)
     assert e.value.status == -3
     assert fiona.lib().fiona_rotation_key_words(None) == 0
+
+
+def test_rescaler_size_limit():
+    """fiona_rescaler_create rejects more ciphertexts than one launch can hold (before touching the device)."""
+    N, L = 256, 2
+    ctx = fiona.Ctx(N, L, synth.ntt_primes(N, L))
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.Rescaler(ctx, 40000)
+    assert e.value.status == -3
