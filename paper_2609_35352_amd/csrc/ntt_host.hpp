@@ -39,9 +39,15 @@ inline uint64_t default_psi(uint32_t N, uint64_t q) {
   return 0;
 }
 
-// Tables of one direction of one modulus.  Forward: pre = psi^n, mid =
-// omega^(n1 k2) at k2 N1 + n1, DFT roots omega^N1 (size N2) and omega^N2
-// (size N1).  Inverse: omega -> omega^-1, no pre, post = N^-1 psi^-k.
+// Tables of one direction of one modulus, for n = n1 + N1 n2 on the input
+// side and k = k2 + N2 k1 on the output side.  Forward: the twist psi^n
+// splits as psi^(N1 n2) psi^n1; pre = psi^(N1 n2) (N2 entries) and the
+// factor psi^n1, constant along pass A's DFT, joins mid = omega^(n1 k2)
+// psi^n1 at k2 N1 + n1.  Inverse (omega -> omega^-1): the factor
+// N^-1 psi^-k = N^-1 psi^-k2 psi^(-N2 k1); the part in k2, constant along
+// pass B's DFT, joins mid = omega^(-n1 k2) N^-1 psi^-k2, and post =
+// psi^(-N2 k1) (N1 entries).  DFT roots omega^N1 (size N2) and omega^N2
+// (size N1).
 struct TableSet {
   std::vector<Tw> pre, mid, dft_a, dft_b, post;
 };
@@ -52,19 +58,25 @@ inline TableSet make_tables(uint32_t log_n1, uint32_t log_n2, uint64_t q, uint64
   const uint64_t omega = inverse ? mulmod_h(psi_inv, psi_inv, q) : mulmod_h(psi, psi, q);
   TableSet t;
   if (!inverse) {
-    t.pre.resize(N);
+    t.pre.resize(N2);
+    const uint64_t step = powmod_h(psi, N1, q);
     uint64_t p = 1;
-    for (uint32_t n = 0; n < N; ++n, p = mulmod_h(p, psi, q)) t.pre[n] = make_tw(p, q);
+    for (uint32_t n2 = 0; n2 < N2; ++n2, p = mulmod_h(p, step, q)) t.pre[n2] = make_tw(p, q);
   } else {
-    t.post.resize(N);
-    uint64_t p = powmod_h(N, q - 2, q);
-    for (uint32_t n = 0; n < N; ++n, p = mulmod_h(p, psi_inv, q)) t.post[n] = make_tw(p, q);
+    t.post.resize(N1);
+    const uint64_t step = powmod_h(psi_inv, N2, q);
+    uint64_t p = 1;
+    for (uint32_t k1 = 0; k1 < N1; ++k1, p = mulmod_h(p, step, q)) t.post[k1] = make_tw(p, q);
   }
   t.mid.resize(N);
+  const uint64_t n_inv = powmod_h(N, q - 2, q);
   for (uint32_t n1 = 0; n1 < N1; ++n1) {
     const uint64_t step = powmod_h(omega, n1, q);
-    uint64_t p = 1;
-    for (uint32_t k2 = 0; k2 < N2; ++k2, p = mulmod_h(p, step, q)) t.mid[(size_t)k2 * N1 + n1] = make_tw(p, q);
+    uint64_t p = inverse ? n_inv : powmod_h(psi, n1, q);   // the k2 = 0 entry
+    for (uint32_t k2 = 0; k2 < N2; ++k2) {
+      t.mid[(size_t)k2 * N1 + n1] = make_tw(p, q);
+      p = mulmod_h(p, inverse ? mulmod_h(step, psi_inv, q) : step, q);
+    }
   }
   const uint64_t w2 = powmod_h(omega, N1, q), w1 = powmod_h(omega, N2, q);
   t.dft_a.resize(N2 / 2);

@@ -133,74 +133,70 @@ struct RotArgs {
 
 template <uint32_t LOGM>
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_b_rot(const NttPass P, const RotArgs R) {
-  constexpr uint32_t M = 1u << LOGM, PM = padded_len(M), PER = kNttCols * M / kNttThreads;
-  constexpr uint32_t B = PER < kNttBatch ? PER : kNttBatch;
+  using D = DftShape<LOGM>;
+  constexpr uint32_t M = D::M, PM = D::PM, PER = kNttCols * M / kNttThreads;
   extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * PM);
   const uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps;
   const uint32_t p = lv / R.n_rot, r = lv - p * R.n_rot;
   const NttSet S = P.sets[set];
   stage_twiddles(tw, S.dft_b, LOGM);
+  Tw t1[8];
+  first_twiddles<LOGM>(t1, S.dft_b);
   const uint32_t log_n2 = P.log_n2, N2 = 1u << log_n2, N = M << log_n2;   // M = N1
   const uint32_t g = R.g[r], cg = (g - 1) / 2, o0 = blockIdx.x * kNttCols;
   const double q = S.q, qinv = S.qinv;
-  const double *tmp = P.tmp + (uint64_t)blockIdx.y * N;
-#pragma unroll
-  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
-    double x[B];
-#pragma unroll
-    for (uint32_t j = 0; j < B; ++j) {
-      const uint32_t idx = threadIdx.x + (b0 + j) * kNttThreads;
-      const uint32_t k2 = (g * (o0 + (idx >> LOGM)) + cg) & (N2 - 1);
-      x[j] = tmp[(size_t)k2 * M + (idx & (M - 1))];
-    }
-#pragma unroll
-    for (uint32_t j = 0; j < B; ++j) {
-      const uint32_t idx = threadIdx.x + (b0 + j) * kNttThreads;
-      xs[(idx >> LOGM) * PM + pidx(bit_reverse(idx & (M - 1), LOGM))] = x[j];
-    }
-  }
-  lds_dft<LOGM>(xs, tw, q, qinv);
-  // row cc of the workgroup (k2 of destination column o0 + cc), k1 = kk + 16 j:
-  // (u' - transform) * P^-1, plus c0 for the first polynomial, back in place
-  const uint32_t cc = threadIdx.x / kNttCols, kk = threadIdx.x % kNttCols;
-  const uint32_t k2c = (g * (o0 + cc) + cg) & (N2 - 1);
-  const uint64_t *base = P.base + set * P.base_set_stride + lv * P.base_stride + (size_t)k2c * M;
-  const uint64_t *add = p == 0 ? P.add + set * P.add_set_stride + (size_t)k2c * M : nullptr;
+  const Buf tmp(P.tmp + (uint64_t)blockIdx.y * N);
 #pragma unroll 1
-  for (uint32_t b0 = 0; b0 < PER; b0 += B) {
-    double y[B];
-    uint64_t bv[B];
+  for (uint32_t it = threadIdx.x; it < D::IT1; it += kNttThreads) {
+    const uint32_t row = it / D::I1, ip = it % D::I1;
+    const uint32_t k2 = (g * (o0 + row) + cg) & (N2 - 1);
+    double x[16];
 #pragma unroll
-    for (uint32_t j = 0; j < B; ++j) bv[j] = base[kk + (b0 + j) * kNttCols];
+    for (uint32_t u = 0; u < 16; ++u) x[u] = tmp.f64((k2 * M + ip) * 8, D::I1 * 8 * bit_reverse(u, 4));
+    first_stages<LOGM>(x, t1, q, qinv);
+    put_first<LOGM>(xs, row, ip, x);
+  }
+  middle_stages<LOGM>(xs, tw, q, qinv);
+  const Buf base(P.base + set * P.base_set_stride + lv * P.base_stride), add(P.add + set * P.add_set_stride);
+  // row cc of the workgroup (k2 of destination column o0 + cc), outputs k1:
+  // (u' - transform) * P^-1, plus c0 for the first polynomial, into LDS
+#pragma unroll 1
+  for (uint32_t it = threadIdx.x; it < D::IT2; it += kNttThreads) {
+    const uint32_t cc = it / D::I2, o = it % D::I2;
+    const uint32_t k2c = (g * (o0 + cc) + cg) & (N2 - 1);
+    double y[D::E2];
+    last_stages<LOGM>(xs, cc, o, tw, y, q, qinv);
+    const uint32_t lane = (k2c * M + o) * 8;   // word k1 = o + (u << S0L) of row k2c
+    uint64_t bv[D::E2];
 #pragma unroll
-    for (uint32_t j = 0; j < B; ++j) {
-      y[j] = xs[cc * PM + pidx(kk + (b0 + j) * kNttCols)];
-      y[j] = canonical(mul_tw(to_f64(bv[j]) - y[j], S.inv, q), q, qinv);
-    }
-    if (add) {
-      uint64_t av[B];
+    for (uint32_t u = 0; u < D::E2; ++u) bv[u] = base.u64(lane, (u << D::S0L) * 8);
 #pragma unroll
-      for (uint32_t j = 0; j < B; ++j) av[j] = add[kk + (b0 + j) * kNttCols];
+    for (uint32_t u = 0; u < D::E2; ++u) y[u] = canonical(mul_tw(to_f64(bv[u]) - y[u], S.inv, q), q, qinv);
+    if (p == 0) {
+      uint64_t av[D::E2];
 #pragma unroll
-      for (uint32_t j = 0; j < B; ++j) {
-        const double z = y[j] + to_f64(av[j]);
-        y[j] = z >= q ? z - q : z;
+      for (uint32_t u = 0; u < D::E2; ++u) av[u] = add.u64(lane, (u << D::S0L) * 8);
+#pragma unroll
+      for (uint32_t u = 0; u < D::E2; ++u) {
+        const double z = y[u] + to_f64(av[u]);
+        y[u] = z >= q ? z - q : z;
       }
     }
 #pragma unroll
-    for (uint32_t j = 0; j < B; ++j) xs[cc * PM + pidx(kk + (b0 + j) * kNttCols)] = y[j];
+    for (uint32_t u = 0; u < D::E2; ++u) xs[cc * PM + pidx(o + (u << D::S0L))] = y[u];
   }
   __syncthreads();
   // destination column o0 + c, rows d_hi = rr + 16 j: runs of 16 words
   const uint32_t c = threadIdx.x % kNttCols, rr = threadIdx.x / kNttCols;
   const uint32_t hi = ((g * (o0 + c) + cg) & (N - 1)) >> log_n2;
-  uint64_t *out = (uint64_t *)P.out + ((size_t)(r * 2 + p) * R.L + set) * N + o0 + c;
+  const Buf out((uint64_t *)P.out + ((size_t)(r * 2 + p) * R.L + set) * N);
+  const uint32_t lane = (o0 + c + rr * N2) * 8;
 #pragma unroll
   for (uint32_t j = 0; j < PER; ++j) {
     const uint32_t d_hi = rr + j * kNttCols;
     const uint32_t k1 = (hi + g * d_hi) & (M - 1);
-    out[(size_t)d_hi * N2] = to_u64(xs[c * PM + pidx(k1)]);
+    out.put(to_u64(xs[c * PM + pidx(k1)]), lane, j * kNttCols * N2 * 8);
   }
 }
 
