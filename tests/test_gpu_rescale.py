@@ -61,6 +61,21 @@ def test_rescale_matches_oracle(dev, N, L, n_ct, seed):
         assert np.array_equal(got[c], want), "ciphertext %d differs" % c
 
 
+@pytest.mark.parametrize("max_ct,launches", [(16384, 4), (10000, 2)])
+def test_rescale_limbs_over_several_launches(dev, max_ct, launches):
+    """A workspace for many ciphertexts limits the limbs per launch pair
+    (65535 vectors per launch): 4 limbs in 4 launch pairs of 1, or in 2 of
+    3 and 1; results as with one launch."""
+    N, L, n_ct = 256, 5, 3
+    assert -(-(L - 1) // min(L - 1, 65535 // (2 * max_ct))) == launches
+    _say("[rescale] N=%d L=%d n_ct=%d max_ct=%d" % (N, L, n_ct, max_ct))
+    moduli = synth.ntt_primes(N, L)
+    cts = _random_cts(n_ct, moduli, N, 17)
+    got = _gpu_rescale(cts, moduli, dev, max_ct=max_ct)
+    for c in range(n_ct):
+        assert np.array_equal(got[c], rs.rescale(cts[c], moduli)), "ciphertext %d differs" % c
+
+
 def test_rescale_boundary_values(dev):
     """Coefficients at the rounding boundary and residues q-1 and 0."""
     N, L = 1 << 10, 3

@@ -217,3 +217,16 @@ def test_rotate_two_output_rounds():
     got, _, _ = _run_gpu(moduli, P, ct, keys, galois, dev)
     for r in (0, 1, 62, 63, 64, 65, 69):
         np.testing.assert_array_equal(got[r], orot.rotate(ct, galois[r], keys[r], moduli, P))
+
+
+def test_rotate_max_rotations():
+    """The most rotations one call takes (256: four rounds of buffered
+    outputs), steps repeating; the round edges checked against the oracle."""
+    dev = _dev()
+    N, L = 256, 2
+    steps = [1 + (i % 127) for i in range(256)]
+    galois = [orot.galois_element(r, N) for r in steps]
+    moduli, P, ct, keys = _random_case(N, L, len(galois), 13)
+    got, _, _ = _run_gpu(moduli, P, ct, keys, galois, dev)
+    for r in (0, 63, 64, 127, 128, 191, 192, 255):
+        np.testing.assert_array_equal(got[r], orot.rotate(ct, galois[r], keys[r], moduli, P))
