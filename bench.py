@@ -129,18 +129,22 @@ def time_layer(layer, dev, steps, warmup, stream, label, flags=0, padded=True):
         for _ in range(warmup):
             fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
         torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(steps):
+        # one event between consecutive launches: the mean over the steps and
+        # each launch's own time (min, median, max) from the same region
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        ev[0].record(stream)
+        for i in range(steps):
             fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
-        e1.record(stream)
+            ev[i + 1].record(stream)
         torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
+        ms = ev[0].elapsed_time(ev[steps]) / steps
+        each = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
         nbytes = synth.algorithmic_bytes(sub)
         total_ms += ms
         total_bytes += nbytes
-        per_chunk.append({"outputs": sub.n_out, "ms": round(ms, 4), "alg_GBps": round(nbytes / ms / 1e6, 1)})
+        per_chunk.append({"outputs": sub.n_out, "ms": round(ms, 4), "alg_GBps": round(nbytes / ms / 1e6, 1),
+                          "ms_min": round(each[0], 4), "ms_median": round(float(np.median(each)), 4),
+                          "ms_max": round(each[-1], 4)})
         st = plan.stats()
         waves.add(st["waves"])
         for key in ("pmult_grouped", "n_use", "addsub_partial", "n_partial", "n_sum_distinct"):
@@ -320,6 +324,27 @@ def cpu_baseline(layer, seconds: float = 10.0):
                       "in %.1f s (inputs generated before timing)" % (n_pos, layer.n_out, layer.cfg.T, passes, t)}
 
 
+def time_mac_microbench(stream, blocks=2048, chunks=200, reps=5):
+    """The register-only rate of the raw route's arithmetic (plaintext words
+    per second, each multiplied into both polynomials), on the stream the
+    kernels run on."""
+    import torch
+    import paper_2609_35352_amd as fiona
+
+    sink = torch.empty(blocks * 256, dtype=torch.int64, device="cuda:0")
+    words = fiona.mac_microbench(blocks, chunks, sink, stream=stream)   # warm-up
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fiona.mac_microbench(blocks, chunks, sink, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"words_per_s": round(words / (ms * 1e-3), 1), "ms_per_launch": round(ms, 4), "words": words,
+            "threads": blocks * 256}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -429,6 +454,11 @@ def main():
     rotate = None
     if args.rotate:
         rotate = time_rotate(layer, dev, args.steps, args.warmup, stream)
+    # the hybrid launch's raw-term multiply-adds against the register-only rate
+    mb = time_mac_microbench(stream)
+    hy_words = layer.n_pm * cfg.L * cfg.N / (hy_ms * 1e-3)
+    mac_rate = {"raw_words_per_s_hybrid": round(hy_words, 1), "raw_words_per_s_register_only": mb["words_per_s"],
+                "frac": round(hy_words / mb["words_per_s"], 4), "microbench": mb}
     wall = time.perf_counter() - t_wall0
 
     traffic = measured_traffic(cfg.name, "hybrid")
@@ -452,6 +482,9 @@ def main():
                    "chunks": n_launch, "seed": args.seed,
                    "pt_pitch_words": hy_pitch, "pt_row_words": cfg.L * cfg.N},
         "achieved_alg_GBps": round(hy_gbs, 1),
+        "launch_ms": {"min": round(sum(c["ms_min"] for c in hy_chunks), 4),
+                      "median": round(sum(c["ms_median"] for c in hy_chunks), 4),
+                      "max": round(sum(c["ms_max"] for c in hy_chunks), 4)},
         "roofline": {"bound": "hbm", "achieved": round(hy_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(hy_gbs / HBM_PEAK_GBS, 4),
                      "traffic": None if traffic is None else round(traffic),
@@ -462,6 +495,7 @@ def main():
         "ablation": ablation,
         "rescale": rescale,
         "rotate": rotate,
+        "mac_rate": mac_rate,
         "gpu_wall_s": round(wall, 2),
     }
     if not args.no_cpu_baseline:

@@ -335,6 +335,25 @@ int fiona_rotation_key_layout(const fiona_rotator *rotator, uint32_t galois, con
 int fiona_hoisted_rotate(const fiona_rotator *rotator, const uint64_t *ct, uint32_t n_rot, const uint32_t *galois,
                          const uint64_t *keys, uint64_t *out_cts, hipStream_t stream);
 
+/*
+ * Measurement helper (not part of the weighted sum): the register-only rate
+ * of the raw route's arithmetic, against which the hybrid kernel's
+ * multiply-add rate is compared.
+ *
+ * fiona_mac_microbench: launches blocks workgroups of 256 threads; every
+ *   thread multiplies chunks * 56 plaintext words held in registers into both
+ *   polynomials' exact accumulators, as the hybrid kernel does for one raw
+ *   term at one position (four 32x32->64 multiply-adds per polynomial, a
+ *   carry step every 56 words), reads no memory, and writes one word to
+ *   sink[thread] (device, blocks * 256 words, caller-owned; the values mean
+ *   nothing).  Asynchronous on stream; allocates nothing.  Errors:
+ *   FIONA_ERR_ARG (blocks or chunks 0, sink NULL), FIONA_ERR_HIP.
+ * fiona_mac_microbench_words: the plaintext words one such launch multiplies
+ *   (blocks * 256 * chunks * 56).
+ */
+int fiona_mac_microbench(uint32_t blocks, uint32_t chunks, uint64_t *sink, hipStream_t stream);
+uint64_t fiona_mac_microbench_words(uint32_t blocks, uint32_t chunks);
+
 /* Static string naming a status code. */
 const char *fiona_status_string(int status);
 

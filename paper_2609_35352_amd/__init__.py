@@ -347,3 +347,18 @@ def hoisted_rotate(rotator: Rotator, ct_t, galois, keys_t, out_t, stream=None) -
     _check(lib().fiona_hoisted_rotate(rotator.handle, _dptr(ct_t, "ct", 8), n_rot, ctypes.cast(g, ctypes.c_void_p),
                                       _dptr(keys_t, "keys", 8), _dptr(out_t, "out_cts", 8), _stream_handle(stream)),
            "fiona_hoisted_rotate")
+
+
+def mac_microbench(blocks: int, chunks: int, sink_t, stream=None) -> int:
+    """fiona_mac_microbench: the register-only raw-route arithmetic over
+    blocks * 256 threads; returns the plaintext words it multiplies."""
+    L = lib()
+    L.fiona_mac_microbench.restype = ctypes.c_int
+    L.fiona_mac_microbench.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p]
+    L.fiona_mac_microbench_words.restype = ctypes.c_uint64
+    L.fiona_mac_microbench_words.argtypes = [ctypes.c_uint32, ctypes.c_uint32]
+    if sink_t.numel() < blocks * 256:
+        raise ValueError("sink holds fewer than blocks * 256 words")
+    _check(L.fiona_mac_microbench(int(blocks), int(chunks), _dptr(sink_t, "sink", 8), _stream_handle(stream)),
+           "fiona_mac_microbench")
+    return int(L.fiona_mac_microbench_words(int(blocks), int(chunks)))
