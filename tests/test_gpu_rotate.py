@@ -230,3 +230,28 @@ def test_rotate_max_rotations():
     got, _, _ = _run_gpu(moduli, P, ct, keys, galois, dev)
     for r in (0, 63, 64, 127, 128, 191, 192, 255):
         np.testing.assert_array_equal(got[r], orot.rotate(ct, galois[r], keys[r], moduli, P))
+
+
+@pytest.mark.parametrize("N,g", [(256, 5), (2048, 2 * 2048 - 1)])
+def test_rotation_key_layout_format(N, g):
+    """The library's key layout word for word, as include/fiona.h documents
+    it: every row of N residues permuted by the rotation's slot map and
+    stored transposed, K'[row][k2 N1 + k1] = K[row][pi^-1(k2 + N2 k1)],
+    pi^-1(i) = (i - (g - 1) / 2) g^-1 mod N."""
+    dev = _dev()
+    L = 2
+    moduli, P, _, keys = _random_case(N, L, 1, 14)
+    ctx = fiona.Ctx(N, L, moduli)
+    rot = fiona.Rotator(ctx, P, 1)
+    kw = rot.key_words()
+    out = torch.empty(kw, dtype=torch.int64, device=dev)
+    fiona.rotation_key_layout(rot, g, _u64(keys[0].reshape(-1), dev), out)
+    torch.cuda.synchronize()
+    got = _host(out, (-1, N))
+    logn = N.bit_length() - 1
+    log_n1, log_n2 = (logn + 1) // 2, logn // 2
+    a = np.arange(N)
+    i = (a >> log_n1) + ((a & ((1 << log_n1) - 1)) << log_n2)   # a = k2 N1 + k1 holds i = k2 + N2 k1
+    src = ((i - (g - 1) // 2) * pow(g, -1, N)) % N
+    np.testing.assert_array_equal(got, keys[0].reshape(-1, N)[:, src])
+
