@@ -45,7 +45,7 @@ typedef enum fiona_status {
   FIONA_ERR_ARG = -1,          /* null pointer, zero or inconsistent size */
   FIONA_ERR_PLAN = -2,         /* layer description inconsistent (index out of range, bad CSR) */
   FIONA_ERR_UNSUPPORTED = -3,  /* N, L or a modulus outside the supported range */
-  FIONA_ERR_ALIGN = -4,        /* a device pointer is not 8-byte aligned */
+  FIONA_ERR_ALIGN = -4,        /* a device pointer is not 8-byte aligned (rotation keys: 16-byte) */
   FIONA_ERR_ALIAS = -5,        /* the output buffer overlaps an input buffer */
   FIONA_ERR_HIP = -6,          /* a HIP runtime call failed (device allocation, copy, launch) */
   FIONA_ERR_NOMEM = -7,        /* host allocation failed */
@@ -315,7 +315,8 @@ int fiona_rescale(const fiona_rescaler *rescaler, const uint64_t *in_cts, uint32
  * fiona_hoisted_rotate: n_rot rotations of one ciphertext.
  *   ct       device, [2][L][N] canonical residues (NTT domain)
  *   galois   host, [n_rot] Galois elements (odd, < 2N; 5^r mod 2N rotates by r)
- *   keys     device, [n_rot] keys in the library layout, key r for galois[r]
+ *   keys     device, [n_rot] keys in the library layout, key r for galois[r];
+ *            16-byte aligned (read 16 bytes per lane)
  *   out_cts  device, [n_rot][2][L][N], overwritten with canonical residues;
  *            must not overlap ct or keys
  *   n_rot    at most the rotator's max_rot

@@ -39,77 +39,98 @@ using namespace fiona_host;
 
 namespace fiona {
 
-constexpr uint32_t kKsTile = 64;    // coefficients per workgroup of the inner product (one per lane)
+constexpr uint32_t kKsTile = 128;   // coefficients per workgroup of the inner product (two per lane)
 constexpr uint32_t kKsWaves = 8;    // wavefronts per workgroup; rotations are dealt out to them
-constexpr uint32_t kKsRoundRot = 64;   // rotations whose outputs are buffered in LDS per round (64 KiB)
+constexpr uint32_t kKsRoundMax = 64;   // rotations whose outputs are buffered in LDS per round, at most
+constexpr size_t kKsLdsMax = 160 * 1024;
 
-// LDS of the inner product: the digits, the zero row and the round's outputs.
-__host__ __device__ constexpr size_t ks_lds_bytes(uint32_t L) {
-  return (size_t)(L + 1) * 64 * sizeof(uint2) + (size_t)kKsRoundRot * 2 * 64 * sizeof(uint64_t);
+typedef uint32_t ks_u4 __attribute__((ext_vector_type(4)));
+typedef uint64_t ks_q2 __attribute__((ext_vector_type(2)));
+
+// LDS of the inner product: the digits, the zero row and `round` rotations'
+// outputs (2 KiB per row of a tile).
+__host__ __device__ constexpr size_t ks_lds_bytes(uint32_t L, uint32_t round) {
+  return (size_t)(L + 1) * kKsTile * sizeof(uint2) + (size_t)round * 2 * kKsTile * sizeof(uint64_t);
+}
+// The most rotations per round that fit the LDS next to the digits.
+inline uint32_t ks_round(uint32_t L) {
+  const size_t free = kKsLdsMax - ks_lds_bytes(L, 0);
+  const size_t r = free / (2 * kKsTile * sizeof(uint64_t));
+  return r < kKsRoundMax ? (uint32_t)r : kKsRoundMax;
 }
 
-// Step 2.  Workgroup = (modulus m, tile of 64 coefficients).  The L digits of
-// the tile are staged in LDS as radix-2^25 digit pairs; each wavefront then
-// takes rotations r = wave, wave + kKsWaves, ..., loads the 2 L key words of
+// Step 2.  Workgroup = (modulus m, tile of 128 coefficients); lane l takes
+// coefficients 2l and 2l + 1 of the tile, so that every key and digit load is
+// 16 bytes per lane and 1 KiB per wavefront.  The L digits of the tile are
+// staged in LDS as radix-2^25 digit pairs; each wavefront then takes
+// rotations r = wave, wave + kKsWaves, ..., loads the 2 L key word pairs of
 // each lane in batches of JB digits (both polynomials), and accumulates the
 // exact products (modarith.hpp), reduced once per output.  Padding terms of a
 // batch read the zero row and repeat a real key address.  The outputs of up
-// to kKsRoundRot rotations wait in LDS and leave together after a barrier
+// to `round` rotations wait in LDS and leave together after a barrier
 // (writes mixed one by one into the key stream cost more: 2-3% measured).
+// Measured against one coefficient per lane (512-byte loads, 2 workgroups
+// per CU): VGG11's 63 rotations 1.75 -> 1.58 ms, BERT's 31 1.67 -> 1.50 ms,
+// Large's 127 10.0 -> 9.5 ms; with one workgroup per CU here (the LDS of a
+// 64-rotation round).
 template <uint32_t JB>
 __global__ void __launch_bounds__(kKsWaves * 64) ks_inner_kernel(const uint64_t *__restrict__ dhat,
                                                                   const uint64_t *__restrict__ keys,
                                                                   uint64_t *__restrict__ u,
                                                                   const LimbConst *__restrict__ limbs, uint32_t N,
-                                                                  uint32_t L, uint32_t n_rot) {
-  extern __shared__ uint2 ks_lds[];   // [L + 1][64] digits of Dhat[j][m] at this tile and a zero row,
-                                      // then [kKsRoundRot][2][64] outputs of a round
-  uint2 *xs = ks_lds;
+                                                                  uint32_t L, uint32_t n_rot, uint32_t round) {
+  extern __shared__ uint4 ks_lds[];   // [L + 1][64] two digit pairs per lane (the last row zero),
+                                      // then [round][2][64] two outputs per lane
+  uint4 *xs = ks_lds;
   const uint32_t tiles = N / kKsTile;
   const uint32_t m = blockIdx.x / tiles, t = blockIdx.x - m * tiles;
   const uint32_t lane = threadIdx.x & 63u, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint32_t k = t * kKsTile + lane;
+  const uint32_t k = t * kKsTile + 2 * lane;
   const uint32_t M = L + 1;
   for (uint32_t j = wave; j < L; j += kKsWaves) {
-    const uint64_t x = __builtin_nontemporal_load(dhat + ((size_t)j * M + m) * N + k);
-    xs[j * 64 + lane] = make_uint2(lo_digit(x), hi_digit(x));
+    const ks_q2 x = __builtin_nontemporal_load((const ks_q2 *)(dhat + ((size_t)j * M + m) * N + k));
+    xs[j * 64 + lane] = make_uint4(lo_digit(x.x), hi_digit(x.x), lo_digit(x.y), hi_digit(x.y));
   }
-  if (wave == 0) xs[L * 64 + lane] = make_uint2(0, 0);
+  if (wave == 0) xs[L * 64 + lane] = make_uint4(0, 0, 0, 0);
   __syncthreads();
   const LimbConst lc = limbs[m];
   const size_t poly = (size_t)M * N;           // words between the two polynomials of a digit
   const size_t rot_words = (size_t)L * 2 * poly;
-  uint64_t *obuf = (uint64_t *)(xs + M * 64);
-  for (uint32_t r0 = 0; r0 < n_rot; r0 += kKsRoundRot) {   // uniform over the workgroup
-    const uint32_t nr = n_rot - r0 < kKsRoundRot ? n_rot - r0 : kKsRoundRot;
+  ks_q2 *obuf = (ks_q2 *)(xs + M * 64);
+  for (uint32_t r0 = 0; r0 < n_rot; r0 += round) {   // uniform over the workgroup
+    const uint32_t nr = n_rot - r0 < round ? n_rot - r0 : round;
     for (uint32_t rr = wave; rr < nr; rr += kKsWaves) {
       const uint64_t *kr = keys + (size_t)(r0 + rr) * rot_words + (size_t)m * N + k;
-      Acc a0, a1;
-      acc_zero(a0);
-      acc_zero(a1);
+      Acc a00, a01, a10, a11;   // [coefficient 2l, 2l + 1][polynomial]
+      acc_zero(a00);
+      acc_zero(a01);
+      acc_zero(a10);
+      acc_zero(a11);
       for (uint32_t j0 = 0; j0 < L; j0 += JB) {
-        uint64_t w0[JB], w1[JB];
+        ks_u4 w0[JB], w1[JB];
 #pragma unroll
         for (uint32_t b = 0; b < JB; ++b) {
           const uint32_t j = j0 + b < L ? j0 + b : L - 1;
-          w0[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly);
-          w1[b] = __builtin_nontemporal_load(kr + (size_t)j * 2 * poly + poly);
+          w0[b] = __builtin_nontemporal_load((const ks_u4 *)(kr + (size_t)j * 2 * poly));
+          w1[b] = __builtin_nontemporal_load((const ks_u4 *)(kr + (size_t)j * 2 * poly + poly));
         }
 #pragma unroll
         for (uint32_t b = 0; b < JB; ++b) {
           const uint32_t row = j0 + b < L ? j0 + b : L;
-          const uint2 x = xs[row * 64 + lane];
-          mac(a0, x.x, x.y, (uint32_t)w0[b], (uint32_t)(w0[b] >> 32));
-          mac(a1, x.x, x.y, (uint32_t)w1[b], (uint32_t)(w1[b] >> 32));
+          const uint4 x = xs[row * 64 + lane];
+          mac(a00, x.x, x.y, w0[b].x, w0[b].y);
+          mac(a01, x.x, x.y, w1[b].x, w1[b].y);
+          mac(a10, x.z, x.w, w0[b].z, w0[b].w);
+          mac(a11, x.z, x.w, w1[b].z, w1[b].w);
         }
       }
-      obuf[(2 * rr) * 64 + lane] = finish(a0, 0, lc);
-      obuf[(2 * rr + 1) * 64 + lane] = finish(a1, 0, lc);
+      obuf[(2 * rr) * 64 + lane] = (ks_q2){finish(a00, 0, lc), finish(a10, 0, lc)};
+      obuf[(2 * rr + 1) * 64 + lane] = (ks_q2){finish(a01, 0, lc), finish(a11, 0, lc)};
     }
     __syncthreads();
     for (uint32_t e = wave; e < 2 * nr; e += kKsWaves) {   // u: [2][n_rot][L + 1][N]
       const uint32_t p = e & 1u, r = r0 + (e >> 1);
-      __builtin_nontemporal_store(obuf[e * 64 + lane], u + (((size_t)p * n_rot + r) * M + m) * N + k);
+      __builtin_nontemporal_store(obuf[e * 64 + lane], (ks_q2 *)(u + (((size_t)p * n_rot + r) * M + m) * N + k));
     }
     __syncthreads();   // the next round refills the buffer
   }
@@ -384,7 +405,7 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
     R->W = (double *)p;
     p += w_bytes;
     R->U = (uint64_t *)p;
-    const int ks_smem = (int)fiona::ks_lds_bytes(L);
+    const int ks_smem = (int)fiona::ks_lds_bytes(L, fiona::ks_round(L));
     const int nt_smem = (int)(fiona::kNttCols * fiona::padded_len(fiona::kNttMaxSide) * sizeof(double) +
                               fiona::kNttMaxSide / 2 * sizeof(Tw));
     if (!allow_smem() ||
@@ -393,7 +414,7 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
         !allow_rot_smem(nt_smem) ||
         hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             ks_smem) != hipSuccess ||
-        hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
+        hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             ks_smem) != hipSuccess) {
       fiona_rotator_destroy(R);
       return FIONA_ERR_HIP;
@@ -443,7 +464,7 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
   const uint32_t N = R->N, L = R->L;
   for (uint32_t r = 0; r < n_rot; ++r)
     if ((galois[r] & 1u) == 0 || galois[r] >= 2 * N) return FIONA_ERR_ARG;
-  if (((uintptr_t)ct | (uintptr_t)keys | (uintptr_t)out_cts) & 7u) return FIONA_ERR_ALIGN;
+  if ((((uintptr_t)ct | (uintptr_t)out_cts) & 7u) || ((uintptr_t)keys & 15u)) return FIONA_ERR_ALIGN;
   const size_t ct_bytes = (size_t)2 * L * N * 8, out_bytes = (size_t)n_rot * ct_bytes;
   const size_t key_bytes = (size_t)n_rot * fiona_rotation_key_words(R) * 8;
   if (overlap(out_cts, out_bytes, ct, ct_bytes) || overlap(out_cts, out_bytes, keys, key_bytes))
@@ -487,14 +508,17 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
                      R->log_n2);
 
   // 2. the inner products of every rotation (transposed layout, pi^-1 frame)
+  //    (batches of 8 digits, or of 4 where that pads fewer: L = 8, 16 take 8, L = 10, 12 take 4)
   const dim3 ks_grid(M * (N / fiona::kKsTile));
-  const size_t ks_smem = fiona::ks_lds_bytes(L);
-  if (L <= 8)
+  const uint32_t round = fiona::ks_round(L);
+  const size_t ks_smem = fiona::ks_lds_bytes(L, round);
+  const uint32_t pad8 = (L + 7) / 8 * 8 - L, pad4 = (L + 3) / 4 * 4 - L;
+  if (pad8 <= pad4)
     hipLaunchKernelGGL(fiona::ks_inner_kernel<8>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat, keys,
-                       R->U, R->limbs, N, L, n_rot);
+                       R->U, R->limbs, N, L, n_rot, round);
   else
-    hipLaunchKernelGGL(fiona::ks_inner_kernel<16>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat,
-                       keys, R->U, R->limbs, N, L, n_rot);
+    hipLaunchKernelGGL(fiona::ks_inner_kernel<4>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat,
+                       keys, R->U, R->limbs, N, L, n_rot, round);
 
   // 3. the division by P: u'_P back to centred coefficients (W), then per
   //    data limb its transform, the subtraction from u', the product with

@@ -166,6 +166,9 @@ def test_rotate_argument_errors():
     with pytest.raises(fiona.FionaError) as e:   # output overlapping the input
         fiona.hoisted_rotate(rot, out[: 2 * L * N], [5], k_t, out)
     assert e.value.status == -5
+    with pytest.raises(fiona.FionaError) as e:   # keys 8 but not 16 bytes aligned
+        fiona.hoisted_rotate(rot, ct_t, [5], k_t[1:], out)
+    assert e.value.status == -4
     fiona.hoisted_rotate(rot, ct_t, [], k_t, out)   # nothing to do
     torch.cuda.synchronize()
 
