@@ -174,7 +174,7 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b_rot(const NttPass P, c
     const uint32_t k2 = (g * (o0 + row) + cg) & (N2 - 1);
     double x[16];
 #pragma unroll
-    for (uint32_t u = 0; u < 16; ++u) x[u] = tmp.f64((k2 * M + ip) * 8, D::I1 * 8 * bit_reverse(u, 4));
+    for (uint32_t u = 0; u < 16; ++u) x[u] = tmp.f64_once((k2 * M + ip) * 8, D::I1 * 8 * bit_reverse(u, 4));
     first_stages<LOGM>(x, t1, q, qinv);
     put_first<LOGM>(xs, row, ip, x);
   }
@@ -191,7 +191,7 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b_rot(const NttPass P, c
     const uint32_t lane = (k2c * M + o) * 8;   // word k1 = o + (u << S0L) of row k2c
     uint64_t bv[D::E2];
 #pragma unroll
-    for (uint32_t u = 0; u < D::E2; ++u) bv[u] = base.u64(lane, (u << D::S0L) * 8);
+    for (uint32_t u = 0; u < D::E2; ++u) bv[u] = base.u64_once(lane, (u << D::S0L) * 8);
 #pragma unroll
     for (uint32_t u = 0; u < D::E2; ++u) y[u] = canonical(mul_tw(to_f64(bv[u]) - y[u], S.inv, q), q, qinv);
     if (p == 0) {
