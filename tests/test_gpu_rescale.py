@@ -90,9 +90,11 @@ def test_rescale_boundary_values(dev):
     assert np.array_equal(got[0], rs.rescale(cts[0], moduli))
 
 
-def test_rescale_full_size(dev):
-    """N = 2^16 with the VGG11-like layer's 8 limbs (the four-step split 256 x 256)."""
-    cfg = synth.CONFIGS["vgg11"]
+@pytest.mark.parametrize("name", ["vgg11", "large4096"])
+def test_rescale_full_size(dev, name):
+    """N = 2^16 with the VGG11-like layer's 8 limbs and the Large layer's 16
+    (the four-step split 256 x 256; 7 and 15 forward limbs in one launch pair)."""
+    cfg = synth.CONFIGS[name]
     moduli = synth.ntt_primes(cfg.N, cfg.L)
     _say("[rescale] full size N=%d L=%d" % (cfg.N, cfg.L))
     cts = _random_cts(1, moduli, cfg.N, 9)
