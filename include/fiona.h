@@ -49,7 +49,9 @@ typedef enum fiona_status {
   FIONA_ERR_ALIAS = -5,        /* the output buffer overlaps an input buffer */
   FIONA_ERR_HIP = -6,          /* a HIP runtime call failed (device allocation, copy, launch) */
   FIONA_ERR_NOMEM = -7,        /* host allocation failed */
-  FIONA_ERR_NODEVICE = -8      /* the plan was created host-only and has no device image */
+  FIONA_ERR_NODEVICE = -8,     /* the plan was created host-only and has no device image */
+  FIONA_ERR_PRECONDITION = -9, /* an input breaks a precondition (checked only where documented) */
+  FIONA_ERR_BOUNDS = -10       /* a replayed access falls outside its buffer (fiona_check_ntt_offsets) */
 } fiona_status;
 
 /* Limits checked by fiona_ctx_create. */
@@ -354,6 +356,30 @@ int fiona_hoisted_rotate(const fiona_rotator *rotator, const uint64_t *ct, uint3
  */
 int fiona_mac_microbench(uint32_t blocks, uint32_t chunks, uint64_t *sink, hipStream_t stream);
 uint64_t fiona_mac_microbench_words(uint32_t blocks, uint32_t chunks);
+
+/*
+ * Checking helper (no device needed): replays the memory accesses of one
+ * rescale (op 0) or one hoisted-rotation call (op 1) on the host.  The
+ * rescaler (capacity = max_ct) or rotator (capacity = max_rot) is laid out
+ * at fake device addresses, the call's launches are recorded instead of
+ * issued, and every global access of every workgroup and thread of every NTT
+ * pass is recomputed with the kernels' own offset arithmetic; the other
+ * kernels of a rotation call are checked by the byte ranges they touch.
+ *   moduli      host, L moduli (op 0) or L data moduli then the special
+ *               prime (op 1), each = 1 mod 2N
+ *   n_call      ciphertexts (op 0) or rotations (op 1) of the call; the
+ *               rotations use Galois elements 5^r, then 2N - 1 and 1
+ *   out_shrink  the caller's output buffer is taken to be this many bytes
+ *               short (0 for the real size; a positive value checks that
+ *               the checker finds the overrun)
+ *   msg         host, msg_len bytes: the first violation, or ""
+ * Returns FIONA_OK if every access lies inside the buffer that holds its
+ * descriptor's base, below 2^32 bytes from it, with every descriptor's end
+ * pointer at that buffer's end; FIONA_ERR_BOUNDS otherwise; the errors of
+ * fiona_rescaler_create / fiona_rotator_create for bad parameters.
+ */
+int fiona_check_ntt_offsets(uint32_t op, uint32_t N, uint32_t L, const uint64_t *moduli, uint32_t capacity,
+                            uint32_t n_call, uint64_t out_shrink, char *msg, size_t msg_len);
 
 /* Static string naming a status code. */
 const char *fiona_status_string(int status);

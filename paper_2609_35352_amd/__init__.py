@@ -30,9 +30,12 @@ FIONA_PLAN_NO_PARTIAL_SHARING = 8
 FIONA_PLAN_PER_CONTRIBUTION = 16
 FIONA_PLAN_NO_OUTPUT_BURSTS = 32
 
+FIONA_ERR_PRECONDITION = -9
+FIONA_ERR_BOUNDS = -10
+
 STATUS = {0: "FIONA_OK", -1: "FIONA_ERR_ARG", -2: "FIONA_ERR_PLAN", -3: "FIONA_ERR_UNSUPPORTED",
           -4: "FIONA_ERR_ALIGN", -5: "FIONA_ERR_ALIAS", -6: "FIONA_ERR_HIP", -7: "FIONA_ERR_NOMEM",
-          -8: "FIONA_ERR_NODEVICE"}
+          -8: "FIONA_ERR_NODEVICE", -9: "FIONA_ERR_PRECONDITION", -10: "FIONA_ERR_BOUNDS"}
 
 
 class FionaError(RuntimeError):
@@ -362,3 +365,19 @@ def mac_microbench(blocks: int, chunks: int, sink_t, stream=None) -> int:
     _check(L.fiona_mac_microbench(int(blocks), int(chunks), _dptr(sink_t, "sink", 8), _stream_handle(stream)),
            "fiona_mac_microbench")
     return int(L.fiona_mac_microbench_words(int(blocks), int(chunks)))
+
+
+def check_ntt_offsets(op: str, N: int, L: int, moduli, capacity: int, n_call: int, out_shrink: int = 0):
+    """fiona_check_ntt_offsets: host replay of every memory access of one
+    rescale (op "rescale", L moduli) or one rotation call (op "rotate", L data
+    moduli then the special prime).  Returns (status, first violation or "")."""
+    L_ = lib()
+    L_.fiona_check_ntt_offsets.restype = ctypes.c_int
+    L_.fiona_check_ntt_offsets.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p,
+                                           ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_char_p,
+                                           ctypes.c_size_t]
+    mods = (ctypes.c_uint64 * len(moduli))(*[int(q) for q in moduli])
+    msg = ctypes.create_string_buffer(512)
+    rc = L_.fiona_check_ntt_offsets({"rescale": 0, "rotate": 1}[op], int(N), int(L), ctypes.cast(mods, ctypes.c_void_p),
+                                    int(capacity), int(n_call), int(out_shrink), msg, 512)
+    return rc, msg.value.decode()

@@ -7,7 +7,8 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRCS = [os.path.join(HERE, "csrc", "fiona.hip"), os.path.join(HERE, "csrc", "rescale.hip"),
-        os.path.join(HERE, "csrc", "rotate.hip"), os.path.join(HERE, "csrc", "microbench.hip")]
+        os.path.join(HERE, "csrc", "rotate.hip"), os.path.join(HERE, "csrc", "microbench.hip"),
+        os.path.join(HERE, "csrc", "ntt_check.hip")]
 OUT = os.path.join(HERE, "libfiona.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -102,11 +102,13 @@ const char *fiona_status_string(int status) {
     case FIONA_ERR_ARG: return "invalid argument";
     case FIONA_ERR_PLAN: return "inconsistent layer description";
     case FIONA_ERR_UNSUPPORTED: return "unsupported size or modulus";
-    case FIONA_ERR_ALIGN: return "device pointer not 8-byte aligned";
+    case FIONA_ERR_ALIGN: return "device pointer not aligned";
     case FIONA_ERR_ALIAS: return "output overlaps an input";
     case FIONA_ERR_HIP: return "HIP runtime error";
     case FIONA_ERR_NOMEM: return "out of host memory";
     case FIONA_ERR_NODEVICE: return "plan has no device image";
+    case FIONA_ERR_PRECONDITION: return "an input breaks a precondition";
+    case FIONA_ERR_BOUNDS: return "a replayed access falls outside its buffer";
     default: return "unknown status";
   }
 }
@@ -218,16 +220,24 @@ void find_partial_sums(std::vector<SumBuild> &sums, const std::vector<uint64_t> 
   std::vector<uint32_t> level_of;   // per partial
   auto level = [&](uint32_t row) { return row < n_in ? 0u : level_of[row - n_in]; };
   std::unordered_map<uint64_t, uint64_t> count;
+  std::vector<uint64_t> keys;
   while (parts.size() < max_rows) {
     count.clear();
     for (size_t s = 0; s < sums.size(); ++s) {
+      // members are sorted by row; a group may name one input twice, and a
+      // pair of one input with itself is no common term.  Each candidate
+      // counts once per sum, as at most one copy of it is replaced there.
       const auto &m = sums[s].members;
+      keys.clear();
       for (size_t i = 0; i < m.size(); ++i)
         for (size_t j = i + 1; j < m.size(); ++j) {
+          if (m[i].row == m[j].row) continue;
           if (std::max(level(m[i].row), level(m[j].row)) + 1 > kMaxPartialLevels) continue;
-          const uint64_t key = ((uint64_t)m[i].row << 33) | ((uint64_t)m[j].row << 1) | (m[i].sign != m[j].sign);
-          count[key] += weight[s];
+          keys.push_back(((uint64_t)m[i].row << 33) | ((uint64_t)m[j].row << 1) | (m[i].sign != m[j].sign));
         }
+      std::sort(keys.begin(), keys.end());
+      keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
+      for (uint64_t key : keys) count[key] += weight[s];
     }
     uint64_t best = 0, best_k = 0;
     for (const auto &kv : count)
@@ -244,12 +254,19 @@ void find_partial_sums(std::vector<SumBuild> &sums, const std::vector<uint64_t> 
     PartialBuild pb;
     for (auto &sb : sums) {
       auto &mm = sb.members;
+      // two distinct members (ra != rb) with this relative sign; with a
+      // repeated input, any copy that fits
       size_t ia = mm.size(), ib = mm.size();
-      for (size_t t = 0; t < mm.size(); ++t) {
-        if (mm[t].row == ra) ia = t;
-        if (mm[t].row == rb) ib = t;
+      for (size_t t = 0; t < mm.size() && ib == mm.size(); ++t) {
+        if (mm[t].row != ra) continue;
+        for (size_t v = 0; v < mm.size(); ++v)
+          if (mm[v].row == rb && mm[t].sign * mm[v].sign == rel) {
+            ia = t;
+            ib = v;
+            break;
+          }
       }
-      if (ia == mm.size() || ib == mm.size() || mm[ia].sign * mm[ib].sign != rel) continue;
+      if (ib == mm.size()) continue;
       if (first_use) {
         pb.first = MemberRef{ra, mm[ia].slot, 1};
         pb.second = MemberRef{rb, mm[ib].slot, rel};
@@ -815,7 +832,8 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   kp.pm = plan->d_pm;
   kp.words = plan->d_words;
   hipLaunchKernelGGL(kernel, dim3(plan->grid), dim3(plan->nw * 64), plan->lds_bytes, stream, in_cts, pt_diags,
-                     out_cts, kp, plan->shape);
+                     out_cts, kp, plan->shape, (const void *)((const char *)pt_diags + pt_bytes),
+                     (const void *)((const char *)out_cts + out_bytes));
   if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   return FIONA_OK;
 }

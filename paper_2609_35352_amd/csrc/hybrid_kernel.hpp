@@ -29,6 +29,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "buffer.hpp"
 #include "modarith.hpp"
 
 namespace fiona {
@@ -221,13 +222,13 @@ __device__ __forceinline__ const uint32_t *sload_block(const uint2 *pm, uint32_t
 }
 
 // All batches of the chunk block blk (uniform address), records in SGPRs:
-// batch b+1 is in flight while batch b is multiplied.
-__device__ __forceinline__ void raw_chunk(const uint32_t *blk, const char *pt_tile, uint32_t voff, Acc &a0, Acc &a1,
-                                          const uint4 *lds, uint32_t lane16) {
+// batch b+1 is in flight while batch b is multiplied.  pt_end: the end of
+// the plaintext table.
+__device__ __forceinline__ void raw_chunk(const uint32_t *blk, const char *pt_tile, const void *pt_end, uint32_t voff,
+                                          Acc &a0, Acc &a1, const uint4 *lds, uint32_t lane16) {
   const uint32_t hlo = sload1(blk + kChunkSlots - 1), hhi = sload1(blk + 2 * kChunkSlots - 1);
   const uint32_t nb = hhi >> 16;
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)(pt_tile + pair64(hlo, hhi & 0xFFFFu)), (short)0, (int)0xFFFFFFFF, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(pt_tile + pair64(hlo, hhi & 0xFFFFu), pt_end);
   u32x2 wa[kRawBatch], wb[kRawBatch];
   raw_issue_s(wa, rs, batch_offsets(blk, 0), voff);
   uint32_t b = 0;
@@ -247,12 +248,13 @@ __device__ __forceinline__ void raw_chunk(const uint32_t *blk, const char *pt_ti
 }
 
 // Stores one output position of both polynomials: row = the output's limb
-// row at this tile (polynomial 0), poly_bytes = the distance to polynomial 1.
-// Nontemporal buffer stores (measured faster than default-policy stores by
-// 13% on a VGG11-sized layer, and than device-scope ones by 2%).
-__device__ __forceinline__ void store_out(uint64_t *row, uint32_t lane_bytes, uint32_t poly_bytes, uint64_t y0,
-                                          uint64_t y1) {
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)row, (short)0, (int)0xFFFFFFFF, 0x00020000);
+// row at this tile (polynomial 0), poly_bytes = the distance to polynomial 1,
+// out_end = the end of the output array.  Nontemporal buffer stores
+// (measured faster than default-policy stores by 13% on a VGG11-sized layer,
+// and than device-scope ones by 2%).
+__device__ __forceinline__ void store_out(uint64_t *row, const void *out_end, uint32_t lane_bytes, uint32_t poly_bytes,
+                                          uint64_t y0, uint64_t y1) {
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(row, out_end);
   __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y0, (uint32_t)(y0 >> 32)}, rs, lane_bytes, 0, kStoreNT);
   __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y1, (uint32_t)(y1 >> 32)}, rs, lane_bytes + poly_bytes, 0,
                                         kStoreNT);
@@ -279,10 +281,11 @@ struct KPlan {
   const uint32_t *words;    // word blocks: common partial sums, resident signed sums, uses
 };
 
+// pt_end, out_end: the ends of the plaintext table and of the output array.
 template <int NW>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4, 4))) hybrid_linear_kernel(
     const uint64_t *__restrict__ in, const uint64_t *__restrict__ pt, uint64_t *__restrict__ out, const KPlan K,
-    const KShape S) {
+    const KShape S, const void *pt_end, const void *out_end) {
   extern __shared__ uint4 lds[];   // [n_in + n_part + n_mat + segment slots + zero row + output buffer][kTile]
   const LimbConst *__restrict__ limbs = K.limbs;
   const uint4 *__restrict__ items = K.items;
@@ -360,7 +363,7 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
         if (c % kFoldChunks == 0) fold(a0, a1, r0, r1, lc);   // keep the accumulators exact
         else { carry(a0); carry(a1); }
       }
-      raw_chunk(sload_block(pm, item.x + c), pt_tile, voff, a0, a1, lds, lane16);
+      raw_chunk(sload_block(pm, item.x + c), pt_tile, pt_end, voff, a0, a1, lds, lane16);
     }
 
     // signed route: each use applies its group's scale once to a signed sum,
@@ -386,7 +389,7 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
       obuf[(d & ~kBufferFlag) * kTile + lane] =
           make_uint4((uint32_t)y0, (uint32_t)(y0 >> 32), (uint32_t)y1, (uint32_t)(y1 >> 32));
     } else if (k < S.N) {
-      store_out(out + (size_t)d * 2 * LN + out_row, lane * 8u, (uint32_t)(LN * 8), y0, y1);
+      store_out(out + (size_t)d * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), y0, y1);
     }
   }
 
@@ -405,13 +408,13 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
       }
       y0 = reduce_i64((int64_t)y0, lc.q, lc.qinv);
       y1 = reduce_i64((int64_t)y1, lc.q, lc.qinv);
-      if (k < S.N) store_out(out + (size_t)sp.x * 2 * LN + out_row, lane * 8u, (uint32_t)(LN * 8), y0, y1);
+      if (k < S.N) store_out(out + (size_t)sp.x * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), y0, y1);
     }
     for (uint32_t e = wave; e < rr.y; e += NW) {
       const uint4 v = obuf[e * kTile + lane];
       const uint32_t j = K.flush[rr.x + e];
       if (k < S.N)
-        store_out(out + (size_t)j * 2 * LN + out_row, lane * 8u, (uint32_t)(LN * 8), pair64(v.x, v.y), pair64(v.z, v.w));
+        store_out(out + (size_t)j * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), pair64(v.x, v.y), pair64(v.z, v.w));
     }
     if (rd + 1 < S.n_rounds) __syncthreads();   // the next round refills the buffer
   }

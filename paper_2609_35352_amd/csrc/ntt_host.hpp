@@ -4,7 +4,9 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include <cstddef>
 #include <cstdint>
+#include <string>
 #include <vector>
 
 #include "ntt_kernel.hpp"
@@ -13,7 +15,55 @@ namespace fiona_host {
 
 using fiona::NttPass;
 using fiona::NttSet;
+using fiona::RotArgs;
 using fiona::Tw;
+
+// A launch as the host replay sees it (ntt_check.hip).  With a recorder
+// installed, the launch helpers below record their launches instead of
+// issuing them; the other kernels of a call record the byte ranges they
+// touch.
+struct PassLaunch {
+  enum Kind : uint32_t { kPassA, kPassB, kPassBRot } kind;
+  uint32_t log_side, log_other, V;   // DFT side, the other side, vectors (gridDim.y)
+  NttPass P;
+  RotArgs G;                         // kPassBRot only
+};
+struct SpanAccess {   // a kernel that is not an NTT pass: bytes [lo, hi) of the buffer at base
+  const char *what;
+  uint64_t base, lo, hi;
+};
+struct LaunchRecord {
+  std::vector<PassLaunch> passes;
+  std::vector<SpanAccess> spans;
+};
+inline LaunchRecord *&launch_recorder() {
+  static thread_local LaunchRecord *rec = nullptr;
+  return rec;
+}
+inline bool record_span(const char *what, const void *base, uint64_t lo, uint64_t hi) {
+  LaunchRecord *rec = launch_recorder();
+  if (!rec) return false;
+  rec->spans.push_back(SpanAccess{what, (uint64_t)base, lo, hi});
+  return true;
+}
+
+// A buffer of the replayed layout: bytes [lo, hi) of a fake address space.
+struct Region {
+  uint64_t lo, hi;
+  std::string name;
+};
+// Checks every access of the recorded launches: each must fall inside the
+// region that holds its descriptor's base, and each descriptor's end pointer
+// must be that region's end.  sets_dev / sets_host: the device address of
+// the table image's NttSet array and its host copy.  Returns "" or the
+// first violation.
+std::string check_launches(const LaunchRecord &rec, const std::vector<Region> &regions, uint64_t sets_dev,
+                           const std::vector<NttSet> &sets_host);
+// The replays of a rescale and of a rotation call (rescale.hip, rotate.hip).
+int rescale_replay(const uint64_t *moduli, uint32_t N, uint32_t L, uint32_t max_ct, uint32_t n_ct,
+                   uint64_t out_shrink, std::string &err);
+int rotate_replay(const uint64_t *moduli, uint32_t N, uint32_t L, uint32_t max_rot, uint32_t n_rot,
+                  uint64_t out_shrink, std::string &err);
 
 inline uint64_t mulmod_h(uint64_t a, uint64_t b, uint64_t q) { return (uint64_t)((unsigned __int128)a * b % q); }
 
@@ -114,21 +164,55 @@ struct TableImage {
   size_t table_bytes() const { return (tw.size() * sizeof(Tw) + 255) / 256 * 256; }
   size_t bytes() const { return table_bytes() + (entries.size() * sizeof(NttSet) + 255) / 256 * 256; }
 
-  // Copies the image to dev (bytes() long); returns the device NttSet array.
-  NttSet *upload(void *dev) const {
+  // The NttSet records of an image placed at device address dev.
+  std::vector<NttSet> sets_at(const void *dev) const {
     const Tw *tb = (const Tw *)dev;
     auto at = [&](size_t o) { return o == (size_t)-1 ? nullptr : tb + o; };
     std::vector<NttSet> sets;
     for (const Entry &e : entries)
       sets.push_back(NttSet{at(e.pre), at(e.mid), at(e.dft_a), at(e.dft_b), at(e.post), e.inv, (double)e.q,
                             1.0 / (double)e.q});
-    NttSet *dsets = (NttSet *)((char *)dev + table_bytes());
+    return sets;
+  }
+  NttSet *sets_addr(void *dev) const { return (NttSet *)((char *)dev + table_bytes()); }
+
+  // Copies the image to dev (bytes() long); returns the device NttSet array.
+  NttSet *upload(void *dev) const {
+    const std::vector<NttSet> sets = sets_at(dev);
+    NttSet *dsets = sets_addr(dev);
     if (hipMemcpy(dev, tw.data(), tw.size() * sizeof(Tw), hipMemcpyHostToDevice) != hipSuccess) return nullptr;
     if (hipMemcpy(dsets, sets.data(), sets.size() * sizeof(NttSet), hipMemcpyHostToDevice) != hipSuccess)
       return nullptr;
     return dsets;
   }
 };
+
+// The regions of an image placed at dev: each table of each set on its own,
+// then the NttSet array.
+inline std::vector<Region> table_regions(const TableImage &img, const void *dev) {
+  std::vector<Region> r;
+  const uint64_t base = (uint64_t)dev;
+  const size_t n = img.tw.size();
+  for (size_t s = 0; s < img.entries.size(); ++s) {
+    const TableImage::Entry &e = img.entries[s];
+    const size_t offs[5] = {e.pre, e.mid, e.dft_a, e.dft_b, e.post};
+    const char *names[5] = {"pre", "mid", "dft_a", "dft_b", "post"};
+    for (int t = 0; t < 5; ++t) {
+      if (offs[t] == (size_t)-1) continue;
+      size_t end = n;   // the next table's start, else the end of the tables
+      for (const TableImage::Entry &f : img.entries) {
+        const size_t o2[5] = {f.pre, f.mid, f.dft_a, f.dft_b, f.post};
+        for (size_t o : o2)
+          if (o != (size_t)-1 && o > offs[t] && o < end) end = o;
+      }
+      r.push_back(Region{base + offs[t] * sizeof(Tw), base + end * sizeof(Tw),
+                         "set " + std::to_string(s) + " " + names[t]});
+    }
+  }
+  r.push_back(Region{base + img.table_bytes(), base + img.table_bytes() + img.entries.size() * sizeof(NttSet),
+                     "NttSet records"});
+  return r;
+}
 
 // The passes are instantiated per DFT side 2^4 .. 2^9.
 template <uint32_t LOG>
@@ -140,6 +224,10 @@ void launch_pair(bool a, dim3 grid, size_t smem, hipStream_t stream, const NttPa
 // One pass over gridDim.y = V vectors (V <= 65535).
 inline void launch_pass(bool a, uint32_t log_side, uint32_t log_other, uint32_t V, hipStream_t stream,
                         const NttPass &P) {
+  if (LaunchRecord *rec = launch_recorder()) {
+    rec->passes.push_back(PassLaunch{a ? PassLaunch::kPassA : PassLaunch::kPassB, log_side, log_other, V, P, {}});
+    return;
+  }
   const dim3 grid((1u << log_other) / fiona::kNttCols, V);
   const size_t smem = fiona::kNttCols * fiona::padded_len(1u << log_side) * sizeof(double) +
                       (1u << log_side) / 2 * sizeof(Tw);

@@ -38,6 +38,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "buffer.hpp"
+
 namespace fiona {
 
 constexpr uint32_t kNttCols = 16;      // columns (pass A) or rows (pass B) per workgroup
@@ -81,25 +83,25 @@ __device__ __forceinline__ uint64_t to_u64(double y) {   // y an integer in [0, 
 }
 
 // A buffer view of global memory for the passes' per-group accesses.  The
-// descriptor holds the base; the byte offset splits into the lane's part (a
-// VGPR) and a part the workgroup shares (an SGPR or a constant), so that the
-// 16 accesses of a group need no vector address arithmetic.  Offsets stay
-// below 2^32 bytes (one vector or one table per view).
+// descriptor holds the base and the bytes left in the buffer; the byte
+// offset splits into the lane's part (a VGPR) and a part the workgroup
+// shares (an SGPR or a constant), so that the 16 accesses of a group need no
+// vector address arithmetic.  Offsets stay below 2^32 bytes (one vector or
+// one table per view).
 typedef uint32_t nv2 __attribute__((ext_vector_type(2)));
 typedef uint32_t nv4 __attribute__((ext_vector_type(4)));
 struct Buf {
   __amdgpu_buffer_rsrc_t rs;
   // p is the same in every lane; readfirstlane keeps the descriptor in SGPRs
-  // where the compiler has computed p in vector registers.
-  __device__ __forceinline__ explicit Buf(const void *p) : rs(make(p)) {}
-  static __device__ __forceinline__ __amdgpu_buffer_rsrc_t make(const void *p) {
+  // where the compiler has computed p in vector registers.  end: the end of
+  // the buffer p points into.
+  __device__ __forceinline__ Buf(const void *p, const void *end) : rs(make(p, end)) {}
+  static __device__ __forceinline__ __amdgpu_buffer_rsrc_t make(const void *p, const void *end) {
     const uint64_t a = (uint64_t)p;
-    // (readfirstlane returns an int: through uint32_t, so that the low half
-    // is not sign-extended into the high half)
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
-    const uint64_t u = ((uint64_t)hi << 32) | lo;
-    return __builtin_amdgcn_make_buffer_rsrc((void *)u, (short)0, (int)0xFFFFFFFF, 0x00020000);
+    // readfirstlane returns an int; join_halves takes it as unsigned
+    const uint64_t u = join_halves((uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)),
+                                   (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a));
+    return __builtin_amdgcn_make_buffer_rsrc((void *)u, (short)0, (int)buffer_extent(u, (uint64_t)end), 0x00020000);
   }
   __device__ __forceinline__ uint64_t u64(uint32_t voff, uint32_t soff) const {
     const nv2 w = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0);
@@ -135,6 +137,10 @@ struct Buf {
 };
 
 __device__ __forceinline__ uint32_t bit_reverse(uint32_t x, uint32_t bits) { return __brev(x) >> (32 - bits); }
+// The four-bit reversal of u < 16 (a group's position in the bit-reversed order).
+__host__ __device__ constexpr uint32_t rev4(uint32_t u) {
+  return ((u & 1u) << 3) | ((u & 2u) << 1) | ((u & 4u) >> 1) | ((u & 8u) >> 3);
+}
 
 // LDS layout of the kNttCols columns.  The 16 lanes of a quarter wave work on
 // the same word of 16 different columns (the DFT's twiddle reads are then
@@ -282,6 +288,7 @@ struct NttSet {
 // set v / vps, whose modulus and tables are sets[v / vps].  Its words sit at
 //   in   + (v / vps) * in_set_stride   + (v % vps) * in_stride   + n,
 // and likewise for out and base; the intermediate of vector v at tmp + v * N.
+// Each buffer's end bounds the descriptors of its accesses (buffer_extent).
 struct NttPass {
   const void *in;        // pass A input
   double *tmp;           // the transposed intermediates
@@ -289,12 +296,133 @@ struct NttPass {
   const uint64_t *base;  // kStoreRescale: residues in [0, q)
   const NttSet *sets;    // device array, one entry per set
   const uint64_t *add;   // ntt_pass_b_rot: residues in [0, q) added to the first polynomials
+  const void *in_end, *tmp_end, *out_end, *base_end, *add_end;   // ends of the buffers above
   uint64_t in_stride, out_stride, base_stride;
   uint64_t in_set_stride, out_set_stride, base_set_stride, add_set_stride;
   uint32_t vps, log_n1, log_n2, load, store;
   uint32_t out_transposed;  // pass B, kStoreU64 and kStoreRescale: write the transposed layout
   uint32_t nsets_shared;   // pass A: 0, or the number of sets when they all read the same input
                            // vectors (in_set_stride 0) and gridDim.x * vps is a multiple of 8
+};
+
+// The passes' global accesses.  These helpers give the work split and the
+// byte offsets of every buffer access (VGPR part v, SGPR part s); the
+// kernels address memory only through them, and the host replay of a
+// launch (ntt_check.hip) runs the same helpers over every workgroup and
+// thread to check each access against the buffer it falls in.
+struct Off {
+  uint32_t v, s;
+};
+
+// Pass A over DFT side N2 = 2^LOGM (other side N1): the unit of workgroup
+// (bx, by) of a grid gx workgroups wide.
+struct UnitA {
+  uint32_t set, lv, cb;
+};
+__host__ __device__ inline UnitA pass_a_unit(uint32_t vps, uint32_t nsets_shared, uint32_t bx, uint32_t by,
+                                             uint32_t gx) {
+  UnitA a;
+  a.set = by / vps;
+  a.lv = by - a.set * vps;
+  a.cb = bx;
+  if (nsets_shared) {
+    // The sets read the same input vectors: give the nsets_shared workgroups
+    // of one (vector, column block) consecutive turns on one XCD (workgroup
+    // ids i, i + 8, ... run there), so that the input is fetched once into
+    // its L2.  The launch covers gx * vps units, a multiple of 8.
+    const uint32_t id = by * gx + bx;
+    const uint32_t u = id >> 3, unit = (id & 7u) + 8u * (u / nsets_shared);
+    a.set = u % nsets_shared;
+    a.lv = unit / gx;
+    a.cb = unit - a.lv * gx;
+  }
+  return a;
+}
+
+template <uint32_t LOGM>
+struct GeomA {
+  using D = DftShape<LOGM>;
+  // first groups, loop index it < IT1: column and group (kLoadU64T walks a column's groups first)
+  static __host__ __device__ uint32_t col(uint32_t it, bool trans) { return trans ? it / D::I1 : it % kNttCols; }
+  static __host__ __device__ uint32_t grp(uint32_t it, bool trans) { return trans ? it % D::I1 : it / kNttCols; }
+  // word u of the first group ip of column n1 (row n2 = ip + I1 rev4(u))
+  static __host__ __device__ Off in(uint32_t n1, uint32_t ip, uint32_t u, uint32_t N1) {
+    return Off{(n1 + N1 * ip) * 8, N1 * D::I1 * 8 * rev4(u)};
+  }
+  // the same element in the transposed layout: n = n1 + N1 n2 at (n mod N2) N1 + n / N2
+  static __host__ __device__ Off in_t(uint32_t n1, uint32_t ip, uint32_t u, uint32_t N1) {
+    const uint32_t n = n1 + N1 * (ip + D::I1 * rev4(u));
+    return Off{((n & (D::M - 1)) * N1 + (n >> LOGM)) * 8, 0};
+  }
+  static __host__ __device__ Off pre(uint32_t ip, uint32_t u) { return Off{ip * 16, D::I1 * 16 * rev4(u)}; }
+  // last groups, loop index it < IT2: column, offset; word u is row k2 = o + (u << S0L)
+  static __host__ __device__ uint32_t col2(uint32_t it) { return it % kNttCols; }
+  static __host__ __device__ uint32_t off2(uint32_t it) { return it / kNttCols; }
+  static __host__ __device__ Off tmp(uint32_t o, uint32_t n1, uint32_t u, uint32_t N1) {
+    return Off{(o * N1 + n1) * 8, ((u << D::S0L) * N1) * 8};
+  }
+  static __host__ __device__ Off mid(uint32_t o, uint32_t n1, uint32_t u, uint32_t N1) {
+    return Off{(o * N1 + n1) * 16, ((u << D::S0L) * N1) * 16};
+  }
+};
+
+// Pass B over DFT side N1 = 2^LOGM (other side N2), workgroup rows r0 .. r0 + 15.
+template <uint32_t LOGM>
+struct GeomB {
+  using D = DftShape<LOGM>;
+  // first groups, it < IT1: row of the workgroup and group; word u from the row's start
+  static __host__ __device__ uint32_t row(uint32_t it) { return it / D::I1; }
+  static __host__ __device__ uint32_t grp(uint32_t it) { return it % D::I1; }
+  static __host__ __device__ Off tmp(uint32_t row, uint32_t ip, uint32_t u) {
+    return Off{(row * D::M + ip) * 8, D::I1 * 8 * rev4(u)};
+  }
+  // last groups, it < IT2: row and offset (out_transposed walks a row's offsets first)
+  static __host__ __device__ uint32_t row2(uint32_t it, bool trans) { return trans ? it / D::I2 : it % kNttCols; }
+  static __host__ __device__ uint32_t off2(uint32_t it, bool trans) { return trans ? it % D::I2 : it / kNttCols; }
+  static __host__ __device__ Off post(uint32_t o, uint32_t u) { return Off{o * 16, (u << D::S0L) * 16}; }
+  // output k2 + N2 k1, k1 = o + (u << S0L), in natural order and transposed
+  static __host__ __device__ Off col(uint32_t k2, uint32_t o, uint32_t u, uint32_t N2) {
+    return Off{(k2 + N2 * o) * 8, (N2 * 8 << D::S0L) * u};
+  }
+  static __host__ __device__ Off row_t(uint32_t k2, uint32_t o, uint32_t u) {
+    return Off{(k2 * D::M + o) * 8, (u << D::S0L) * 8};
+  }
+};
+
+// The fused pass B of the rotations (ntt_pass_b_rot, rotate.hip) over DFT
+// side N1 = 2^LOGM: destination columns d_lo = o0 .. o0 + 15 of the rotation
+// by Galois element g.
+constexpr uint32_t kRotMax = 256;   // rotations per call (their Galois elements ride in the arguments)
+
+struct RotArgs {
+  uint32_t g[kRotMax];
+  uint32_t n_rot, L;
+};
+
+template <uint32_t LOGM>
+struct GeomRot {
+  using D = DftShape<LOGM>;
+  static constexpr uint32_t PER = kNttCols * D::M / kNttThreads;   // stores per thread
+  // first groups, it < IT1: the workgroup's column and group
+  static __host__ __device__ uint32_t row(uint32_t it) { return it / D::I1; }
+  static __host__ __device__ uint32_t grp(uint32_t it) { return it % D::I1; }
+  // the intermediate row k2 that destination column d_lo reads
+  static __host__ __device__ uint32_t src_row(uint32_t g, uint32_t d_lo, uint32_t N2) {
+    return (g * d_lo + (g - 1) / 2) & (N2 - 1);
+  }
+  static __host__ __device__ Off tmp(uint32_t k2, uint32_t ip, uint32_t u) {
+    return Off{(k2 * D::M + ip) * 8, D::I1 * 8 * rev4(u)};
+  }
+  // last groups, it < IT2: the workgroup's column and offset; word k1 = o + (u << S0L) of row k2
+  static __host__ __device__ uint32_t row2(uint32_t it) { return it / D::I2; }
+  static __host__ __device__ uint32_t off2(uint32_t it) { return it % D::I2; }
+  static __host__ __device__ Off word(uint32_t k2, uint32_t o, uint32_t u) {
+    return Off{(k2 * D::M + o) * 8, (u << D::S0L) * 8};
+  }
+  // store j of thread t: column o0 + t mod 16, destination row d_hi = t / 16 + 16 j
+  static __host__ __device__ Off out(uint32_t o0, uint32_t t, uint32_t j, uint32_t N2) {
+    return Off{(o0 + t % kNttCols + (t / kNttCols) * N2) * 8, j * kNttCols * N2 * 8};
+  }
 };
 
 // Pass A, N2 = 2^LOGM: grid (N1 / kNttCols, vectors).  The first groups of
@@ -305,20 +433,11 @@ struct NttPass {
 template <uint32_t LOGM>
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
   using D = DftShape<LOGM>;
+  using G = GeomA<LOGM>;
   extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * D::PM);
-  uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps, cb = blockIdx.x;
-  if (P.nsets_shared) {
-    // The sets read the same input vectors: give the nsets_shared workgroups
-    // of one (vector, column block) consecutive turns on one XCD (workgroup
-    // ids i, i + 8, ... run there), so that the input is fetched once into
-    // its L2.  The launch covers gridDim.x * vps units, a multiple of 8.
-    const uint32_t id = blockIdx.y * gridDim.x + blockIdx.x;
-    const uint32_t u = id >> 3, unit = (id & 7u) + 8u * (u / P.nsets_shared);
-    set = u % P.nsets_shared;
-    lv = unit / gridDim.x;
-    cb = unit - lv * gridDim.x;
-  }
+  const UnitA un = pass_a_unit(P.vps, P.nsets_shared, blockIdx.x, blockIdx.y, gridDim.x);
+  const uint32_t set = un.set, lv = un.lv, cb = un.cb;
   const NttSet S = P.sets[set];
   stage_twiddles(tw, S.dft_a, LOGM);
   Tw t1[8];
@@ -328,38 +447,45 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
   const uint64_t in_off = set * P.in_set_stride + lv * P.in_stride;
   const double q = S.q, qinv = S.qinv;
   const bool trans = P.load == kLoadU64T;   // uniform
-  const Buf in((const char *)P.in + in_off * 8);
-  const uint32_t row_step = N1 * D::I1 * 8;   // bytes between the group's rows n2 and n2 + I1
+  const Buf in((const char *)P.in + in_off * 8, P.in_end);
 #pragma unroll 1
   for (uint32_t it = threadIdx.x; it < D::IT1; it += kNttThreads) {
-    const uint32_t cl = trans ? it / D::I1 : it % kNttCols, ip = trans ? it % D::I1 : it / kNttCols;
+    const uint32_t cl = G::col(it, trans), ip = G::grp(it, trans);
     const uint32_t n1 = cb * kNttCols + cl;
     double r[16];
-    if (trans) {   // element n = n1 + N1 n2 sits at (n mod N2) N1 + n / N2; no pre
+    if (trans) {   // no pre
       uint64_t w[16];
 #pragma unroll
       for (uint32_t u = 0; u < 16; ++u) {
-        const uint32_t n = n1 + N1 * (ip + D::I1 * bit_reverse(u, 4));
-        w[u] = in.u64(((n & (N2 - 1)) * N1 + (n >> LOGM)) * 8, 0);
+        const Off o = G::in_t(n1, ip, u, N1);
+        w[u] = in.u64(o.v, o.s);
       }
 #pragma unroll
       for (uint32_t u = 0; u < 16; ++u) r[u] = reduce(to_f64(w[u]), q, qinv);
     } else {
-      const uint32_t lane = (n1 + N1 * ip) * 8;
       if (P.load == kLoadF64) {
 #pragma unroll
-        for (uint32_t u = 0; u < 16; ++u) r[u] = in.f64(lane, row_step * bit_reverse(u, 4));
+        for (uint32_t u = 0; u < 16; ++u) {
+          const Off o = G::in(n1, ip, u, N1);
+          r[u] = in.f64(o.v, o.s);
+        }
       } else {
         uint64_t w[16];
 #pragma unroll
-        for (uint32_t u = 0; u < 16; ++u) w[u] = in.u64(lane, row_step * bit_reverse(u, 4));
+        for (uint32_t u = 0; u < 16; ++u) {
+          const Off o = G::in(n1, ip, u, N1);
+          w[u] = in.u64(o.v, o.s);
+        }
 #pragma unroll
         for (uint32_t u = 0; u < 16; ++u) r[u] = to_f64(w[u]);
       }
       if (S.pre) {
-        const Buf pre(S.pre);
+        const Buf pre(S.pre, S.pre + N2);
 #pragma unroll
-        for (uint32_t u = 0; u < 16; ++u) r[u] = mul_tw(r[u], pre.tw(ip * 16, D::I1 * 16 * bit_reverse(u, 4)), q);
+        for (uint32_t u = 0; u < 16; ++u) {
+          const Off o = G::pre(ip, u);
+          r[u] = mul_tw(r[u], pre.tw(o.v, o.s), q);
+        }
       } else {
 #pragma unroll
         for (uint32_t u = 0; u < 16; ++u) r[u] = reduce(r[u], q, qinv);
@@ -369,17 +495,16 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
     put_first<LOGM>(xs, cl, ip, r);
   }
   middle_stages<LOGM>(xs, tw, q, qinv);
-  const Buf tmp(P.tmp + v * ((uint64_t)N1 * N2)), mid(S.mid);
+  const Buf tmp(P.tmp + v * ((uint64_t)N1 * N2), P.tmp_end), mid(S.mid, S.mid + (size_t)N1 * N2);
 #pragma unroll 1
   for (uint32_t it = threadIdx.x; it < D::IT2; it += kNttThreads) {
-    const uint32_t cl = it % kNttCols, o = it / kNttCols, n1 = cb * kNttCols + cl;
+    const uint32_t cl = G::col2(it), o = G::off2(it), n1 = cb * kNttCols + cl;
     double r[D::E2];
     last_stages<LOGM>(xs, cl, o, tw, r, q, qinv);
-    const uint32_t k = o * N1 + n1;   // the word k2 N1 + n1 of row k2 = o + (u << S0L)
 #pragma unroll
     for (uint32_t u = 0; u < D::E2; ++u) {
-      const uint32_t ku = (u << D::S0L) * N1;
-      tmp.put(mul_tw(r[u], mid.tw(k * 16, ku * 16), q), k * 8, ku * 8);
+      const Off om = G::mid(o, n1, u, N1), ot = G::tmp(o, n1, u, N1);
+      tmp.put(mul_tw(r[u], mid.tw(om.v, om.s), q), ot.v, ot.s);
     }
   }
 }
@@ -391,6 +516,7 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_a(const NttPass P) {
 template <uint32_t LOGM>
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
   using D = DftShape<LOGM>;
+  using G = GeomB<LOGM>;
   extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * D::PM);
   const uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps;
@@ -401,51 +527,69 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b(const NttPass P) {
   const uint32_t N2 = 1u << P.log_n2, r0 = blockIdx.x * kNttCols, M = D::M;
   const uint64_t v = blockIdx.y;
   const double q = S.q, qinv = S.qinv;
-  const Buf tmp(P.tmp + v * ((uint64_t)N2 * M) + (size_t)r0 * M);
+  const Buf tmp(P.tmp + v * ((uint64_t)N2 * M) + (size_t)r0 * M, P.tmp_end);
 #pragma unroll 1
   for (uint32_t it = threadIdx.x; it < D::IT1; it += kNttThreads) {
-    const uint32_t row = it / D::I1, ip = it % D::I1;
+    const uint32_t row = G::row(it), ip = G::grp(it);
     double r[16];
 #pragma unroll
-    for (uint32_t u = 0; u < 16; ++u) r[u] = tmp.f64_once((row * M + ip) * 8, D::I1 * 8 * bit_reverse(u, 4));
+    for (uint32_t u = 0; u < 16; ++u) {
+      const Off o = G::tmp(row, ip, u);
+      r[u] = tmp.f64_once(o.v, o.s);
+    }
     first_stages<LOGM>(r, t1, q, qinv);
     put_first<LOGM>(xs, row, ip, r);
   }
   middle_stages<LOGM>(xs, tw, q, qinv);
   const bool transposed = P.out_transposed != 0 && P.store != kStoreF64;   // uniform
   const bool rescale = P.store == kStoreRescale;
-  const Buf out((const char *)P.out + (set * P.out_set_stride + lv * P.out_stride) * 8);
-  const Buf base(rescale ? P.base + set * P.base_set_stride + lv * P.base_stride : nullptr);
-  const uint32_t col_step = N2 * 8 << D::S0L;   // bytes between outputs k1 and k1 + 2^S0L of one column
+  const Buf out((const char *)P.out + (set * P.out_set_stride + lv * P.out_stride) * 8, P.out_end);
+  const Buf base(rescale ? P.base + set * P.base_set_stride + lv * P.base_stride : nullptr,
+                 rescale ? P.base_end : nullptr);
 #pragma unroll 1
   for (uint32_t it = threadIdx.x; it < D::IT2; it += kNttThreads) {
-    const uint32_t row = transposed ? it / D::I2 : it % kNttCols, o = transposed ? it % D::I2 : it / kNttCols;
-    const uint32_t k2 = r0 + row, lane = (k2 + N2 * o) * 8;   // output k2 + N2 k1, k1 = o + (u << S0L)
+    const uint32_t row = G::row2(it, transposed), o = G::off2(it, transposed);
+    const uint32_t k2 = r0 + row;   // output k2 + N2 k1, k1 = o + (u << S0L)
     double y[D::E2];
     last_stages<LOGM>(xs, row, o, tw, y, q, qinv);
     if (S.post) {
-      const Buf post(S.post);
+      const Buf post(S.post, S.post + M);
 #pragma unroll
-      for (uint32_t u = 0; u < D::E2; ++u) y[u] = mul_tw(y[u], post.tw(o * 16, (u << D::S0L) * 16), q);
+      for (uint32_t u = 0; u < D::E2; ++u) {
+        const Off op = G::post(o, u);
+        y[u] = mul_tw(y[u], post.tw(op.v, op.s), q);
+      }
     }
     if (P.store == kStoreF64) {
 #pragma unroll
-      for (uint32_t u = 0; u < D::E2; ++u) out.put(reduce(y[u], q, qinv), lane, col_step * u);
+      for (uint32_t u = 0; u < D::E2; ++u) {
+        const Off oc = G::col(k2, o, u, N2);
+        out.put(reduce(y[u], q, qinv), oc.v, oc.s);
+      }
       continue;
     }
     if (rescale) {
       uint64_t bv[D::E2];
 #pragma unroll
-      for (uint32_t u = 0; u < D::E2; ++u) bv[u] = base.u64_once(lane, col_step * u);
+      for (uint32_t u = 0; u < D::E2; ++u) {
+        const Off oc = G::col(k2, o, u, N2);
+        bv[u] = base.u64_once(oc.v, oc.s);
+      }
 #pragma unroll
       for (uint32_t u = 0; u < D::E2; ++u) y[u] = mul_tw(to_f64(bv[u]) - y[u], S.inv, q);
     }
     if (transposed) {
 #pragma unroll
-      for (uint32_t u = 0; u < D::E2; ++u) out.put(to_u64(canonical(y[u], q, qinv)), (k2 * M + o) * 8, (u << D::S0L) * 8);
+      for (uint32_t u = 0; u < D::E2; ++u) {
+        const Off ot = G::row_t(k2, o, u);
+        out.put(to_u64(canonical(y[u], q, qinv)), ot.v, ot.s);
+      }
     } else {
 #pragma unroll
-      for (uint32_t u = 0; u < D::E2; ++u) out.put(to_u64(canonical(y[u], q, qinv)), lane, col_step * u);
+      for (uint32_t u = 0; u < D::E2; ++u) {
+        const Off oc = G::col(k2, o, u, N2);
+        out.put(to_u64(canonical(y[u], q, qinv)), oc.v, oc.s);
+      }
     }
   }
 }

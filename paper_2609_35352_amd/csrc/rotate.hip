@@ -145,17 +145,11 @@ __global__ void __launch_bounds__(kKsWaves * 64) ks_inner_kernel(const uint64_t 
 // in the transposed layout, so row k2 is contiguous too), and then stores
 // each destination row d_hi as a run of 16 words, picking k1 in LDS.
 // Vectors: set = data limb l, vector lv = p n_rot + r in the set.
-constexpr uint32_t kRotMax = 256;   // rotations per call (their Galois elements ride in the arguments)
-
-struct RotArgs {
-  uint32_t g[kRotMax];
-  uint32_t n_rot, L;
-};
-
 template <uint32_t LOGM>
 __global__ void __launch_bounds__(kNttThreads) ntt_pass_b_rot(const NttPass P, const RotArgs R) {
   using D = DftShape<LOGM>;
-  constexpr uint32_t M = D::M, PM = D::PM, PER = kNttCols * M / kNttThreads;
+  using G = GeomRot<LOGM>;
+  constexpr uint32_t M = D::M, PM = D::PM, PER = G::PER;
   extern __shared__ double xs[];   // [kNttCols][PM], then the M/2 DFT twiddles
   Tw *tw = (Tw *)(xs + kNttCols * PM);
   const uint32_t set = blockIdx.y / P.vps, lv = blockIdx.y - set * P.vps;
@@ -167,37 +161,46 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b_rot(const NttPass P, c
   const uint32_t log_n2 = P.log_n2, N2 = 1u << log_n2, N = M << log_n2;   // M = N1
   const uint32_t g = R.g[r], cg = (g - 1) / 2, o0 = blockIdx.x * kNttCols;
   const double q = S.q, qinv = S.qinv;
-  const Buf tmp(P.tmp + (uint64_t)blockIdx.y * N);
+  const Buf tmp(P.tmp + (uint64_t)blockIdx.y * N, P.tmp_end);
 #pragma unroll 1
   for (uint32_t it = threadIdx.x; it < D::IT1; it += kNttThreads) {
-    const uint32_t row = it / D::I1, ip = it % D::I1;
-    const uint32_t k2 = (g * (o0 + row) + cg) & (N2 - 1);
+    const uint32_t row = G::row(it), ip = G::grp(it);
+    const uint32_t k2 = G::src_row(g, o0 + row, N2);
     double x[16];
 #pragma unroll
-    for (uint32_t u = 0; u < 16; ++u) x[u] = tmp.f64_once((k2 * M + ip) * 8, D::I1 * 8 * bit_reverse(u, 4));
+    for (uint32_t u = 0; u < 16; ++u) {
+      const Off ot = G::tmp(k2, ip, u);
+      x[u] = tmp.f64_once(ot.v, ot.s);
+    }
     first_stages<LOGM>(x, t1, q, qinv);
     put_first<LOGM>(xs, row, ip, x);
   }
   middle_stages<LOGM>(xs, tw, q, qinv);
-  const Buf base(P.base + set * P.base_set_stride + lv * P.base_stride), add(P.add + set * P.add_set_stride);
+  const Buf base(P.base + set * P.base_set_stride + lv * P.base_stride, P.base_end),
+      add(P.add + set * P.add_set_stride, P.add_end);
   // row cc of the workgroup (k2 of destination column o0 + cc), outputs k1:
   // (u' - transform) * P^-1, plus c0 for the first polynomial, into LDS
 #pragma unroll 1
   for (uint32_t it = threadIdx.x; it < D::IT2; it += kNttThreads) {
-    const uint32_t cc = it / D::I2, o = it % D::I2;
-    const uint32_t k2c = (g * (o0 + cc) + cg) & (N2 - 1);
+    const uint32_t cc = G::row2(it), o = G::off2(it);
+    const uint32_t k2c = G::src_row(g, o0 + cc, N2);
     double y[D::E2];
     last_stages<LOGM>(xs, cc, o, tw, y, q, qinv);
-    const uint32_t lane = (k2c * M + o) * 8;   // word k1 = o + (u << S0L) of row k2c
     uint64_t bv[D::E2];
 #pragma unroll
-    for (uint32_t u = 0; u < D::E2; ++u) bv[u] = base.u64_once(lane, (u << D::S0L) * 8);
+    for (uint32_t u = 0; u < D::E2; ++u) {
+      const Off ow = G::word(k2c, o, u);
+      bv[u] = base.u64_once(ow.v, ow.s);
+    }
 #pragma unroll
     for (uint32_t u = 0; u < D::E2; ++u) y[u] = canonical(mul_tw(to_f64(bv[u]) - y[u], S.inv, q), q, qinv);
     if (p == 0) {
       uint64_t av[D::E2];
 #pragma unroll
-      for (uint32_t u = 0; u < D::E2; ++u) av[u] = add.u64(lane, (u << D::S0L) * 8);
+      for (uint32_t u = 0; u < D::E2; ++u) {
+        const Off ow = G::word(k2c, o, u);
+        av[u] = add.u64(ow.v, ow.s);
+      }
 #pragma unroll
       for (uint32_t u = 0; u < D::E2; ++u) {
         const double z = y[u] + to_f64(av[u]);
@@ -211,13 +214,13 @@ __global__ void __launch_bounds__(kNttThreads) ntt_pass_b_rot(const NttPass P, c
   // destination column o0 + c, rows d_hi = rr + 16 j: runs of 16 words
   const uint32_t c = threadIdx.x % kNttCols, rr = threadIdx.x / kNttCols;
   const uint32_t hi = ((g * (o0 + c) + cg) & (N - 1)) >> log_n2;
-  const Buf out((uint64_t *)P.out + ((size_t)(r * 2 + p) * R.L + set) * N);
-  const uint32_t lane = (o0 + c + rr * N2) * 8;
+  const Buf out((uint64_t *)P.out + ((size_t)(r * 2 + p) * R.L + set) * N, P.out_end);
 #pragma unroll
   for (uint32_t j = 0; j < PER; ++j) {
     const uint32_t d_hi = rr + j * kNttCols;
     const uint32_t k1 = (hi + g * d_hi) & (M - 1);
-    out.put(to_u64(xs[c * PM + pidx(k1)]), lane, j * kNttCols * N2 * 8);
+    const Off oo = G::out(o0, threadIdx.x, j, N2);
+    out.put(to_u64(xs[c * PM + pidx(k1)]), oo.v, oo.s);
   }
 }
 
@@ -268,6 +271,9 @@ struct fiona_rotator {
   double *T = nullptr;                 // NTT intermediates: max(L (L + 1), 2 L max_rot) vectors
   double *W = nullptr;                 // [2 max_rot][N] centred coefficients of u'_P
   uint64_t *U = nullptr;               // [2][n_rot][L + 1][N], transposed layout
+  const void *D_end = nullptr, *Dhat_end = nullptr, *c0t_end = nullptr, *T_end = nullptr, *W_end = nullptr,
+             *U_end = nullptr;
+  size_t limb_bytes = 0;
 };
 
 namespace {
@@ -282,6 +288,10 @@ void launch_rot_b(dim3 grid, size_t smem, hipStream_t stream, const NttPass &P, 
 // The fused pass B over V vectors: grid (N2 / 16 destination blocks, V).
 void launch_rot_pass_b(uint32_t log_n1, uint32_t log_n2, uint32_t V, hipStream_t stream, const NttPass &P,
                        const fiona::RotArgs &G) {
+  if (LaunchRecord *rec = launch_recorder()) {
+    rec->passes.push_back(PassLaunch{PassLaunch::kPassBRot, log_n1, log_n2, V, P, G});
+    return;
+  }
   const dim3 grid((1u << log_n2) / fiona::kNttCols, V);
   const size_t smem = fiona::kNttCols * fiona::padded_len(1u << log_n1) * sizeof(double) +
                       (1u << log_n1) / 2 * sizeof(Tw);
@@ -311,15 +321,11 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
   return a0 < b0 + nb && b0 < a0 + na;
 }
 
-}  // namespace
-
-extern "C" {
-
-int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uint64_t *psi, uint32_t max_rot,
-                         fiona_rotator **out) {
-  if (!out) return FIONA_ERR_ARG;
-  *out = nullptr;
-  if (!ctx || max_rot == 0) return FIONA_ERR_ARG;
+// Checks the parameters and sizes a rotator: its tables (img) and the bytes
+// of its device buffer.  R->ext (host only) is created here.
+int rotator_layout(const fiona_ctx *ctx, uint64_t special_prime, const uint64_t *psi, uint32_t max_rot,
+                   fiona_rotator *R, TableImage &img, size_t &total) {
+  if (max_rot == 0) return FIONA_ERR_ARG;
   const uint32_t N = ctx->N, L = ctx->L;
   uint32_t logN = 0;
   while ((1u << logN) < N) ++logN;
@@ -339,8 +345,6 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
     roots[i] = psi ? psi[i] % q : default_psi(N, q);
     if (roots[i] == 0 || powmod_h(roots[i], N, q) != q - 1) return FIONA_ERR_UNSUPPORTED;
   }
-  fiona_rotator *R = new (std::nothrow) fiona_rotator;
-  if (!R) return FIONA_ERR_NOMEM;
   R->ctx = ctx;
   R->N = N;
   R->L = L;
@@ -348,70 +352,275 @@ int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uin
   R->log_n1 = (logN + 1) / 2;
   R->log_n2 = logN / 2;
   R->max_rot = max_rot;
-  int rc = fiona_ctx_create(N, L + 1, mods.data(), &R->ext);
+  const int rc = fiona_ctx_create(N, L + 1, mods.data(), &R->ext);
+  if (rc != FIONA_OK) return rc;
+  for (uint32_t j = 0; j < L; ++j) img.add(make_tables(R->log_n1, R->log_n2, mods[j], roots[j], true), mods[j]);
+  for (uint32_t i = 0; i <= L; ++i) img.add(make_tables(R->log_n1, R->log_n2, mods[i], roots[i], false), mods[i]);
+  for (uint32_t l = 0; l < L; ++l)
+    img.add(make_tables(R->log_n1, R->log_n2, mods[l], roots[l], false), mods[l],
+            make_tw(powmod_h(P % mods[l], mods[l] - 2, mods[l]), mods[l]));
+  img.add(make_tables(R->log_n1, R->log_n2, P, roots[L], true), P);
+  const size_t vec = (size_t)N * 8;
+  R->limb_bytes = round256((L + 1) * sizeof(fiona::LimbConst));
+  const size_t t_vectors = std::max((size_t)L * (L + 1), (size_t)2 * L * max_rot);
+  total = img.bytes() + R->limb_bytes + round256(L * vec) + round256((size_t)L * (L + 1) * vec) +
+          round256(L * vec) + round256(t_vectors * vec) + round256((size_t)2 * max_rot * vec) +
+          round256((size_t)max_rot * 2 * (L + 1) * vec);
+  return FIONA_OK;
+}
+
+// Points the rotator's parts into its device buffer at dev.
+void rotator_place(fiona_rotator *R, const TableImage &img, void *dev) {
+  const uint32_t L = R->L;
+  const size_t vec = (size_t)R->N * 8;
+  const size_t t_vectors = std::max((size_t)L * (L + 1), (size_t)2 * L * R->max_rot);
+  R->dev = dev;
+  const NttSet *sets = img.sets_addr(dev);
+  R->inv_sets = sets;
+  R->fwd_sets = sets + L;
+  R->down_sets = sets + 2 * L + 1;
+  R->p_inv_set = sets + 3 * L + 1;
+  char *p = (char *)dev + img.bytes();
+  auto take = [&](size_t bytes, const void *&end) {
+    char *at = p;
+    end = at + bytes;
+    p += round256(bytes);
+    return at;
+  };
+  const void *limbs_end = nullptr;
+  R->limbs = (const fiona::LimbConst *)take((L + 1) * sizeof(fiona::LimbConst), limbs_end);
+  R->D = (uint64_t *)take(L * vec, R->D_end);
+  R->Dhat = (uint64_t *)take((size_t)L * (L + 1) * vec, R->Dhat_end);
+  R->c0t = (uint64_t *)take(L * vec, R->c0t_end);
+  R->T = (double *)take(t_vectors * vec, R->T_end);
+  R->W = (double *)take((size_t)2 * R->max_rot * vec, R->W_end);
+  R->U = (uint64_t *)take((size_t)R->max_rot * 2 * (L + 1) * vec, R->U_end);
+}
+
+// The launches of one call (arguments already checked).
+void rotate_enqueue(const fiona_rotator *R, const uint64_t *ct, uint32_t n_rot, const uint32_t *galois,
+                    const uint64_t *keys, uint64_t *out_cts, hipStream_t stream) {
+  const uint32_t N = R->N, L = R->L;
+  const uint32_t M = L + 1;
+  const void *ct_end = ct + (size_t)2 * L * N, *out_end = out_cts + (size_t)n_rot * 2 * L * N;
+
+  // 1. digits of c1, once: D_j = INTT_{q_j}(c1_j), then Dhat[j][m] = NTT_m(D_j)
+  //    (transposed layout); c0 transposed for step 3
+  NttPass A{};
+  A.sets = R->inv_sets;
+  A.vps = 1;
+  A.log_n1 = R->log_n1;
+  A.log_n2 = R->log_n2;
+  A.in = ct + (size_t)L * N;
+  A.in_end = ct_end;
+  A.in_set_stride = N;
+  A.tmp = R->T;
+  A.tmp_end = R->T_end;
+  A.out = R->D;
+  A.out_end = R->D_end;
+  A.out_set_stride = N;
+  A.load = fiona::kLoadU64;
+  A.store = fiona::kStoreU64;
+  launch_transform(R->log_n1, R->log_n2, L, stream, A);
+  NttPass B{};
+  B.sets = R->fwd_sets;
+  B.vps = L;
+  B.log_n1 = R->log_n1;
+  B.log_n2 = R->log_n2;
+  B.in = R->D;
+  B.in_end = R->D_end;
+  B.in_stride = N;
+  B.tmp = R->T;
+  B.tmp_end = R->T_end;
+  B.out = R->Dhat;
+  B.out_end = R->Dhat_end;
+  B.out_stride = (size_t)M * N;
+  B.out_set_stride = N;
+  B.load = fiona::kLoadU64;
+  B.store = fiona::kStoreU64;
+  B.out_transposed = 1;
+  B.nsets_shared = ((1u << R->log_n1) / fiona::kNttCols * L) % 8 == 0 ? M : 0;   // every modulus reads D_j
+  launch_transform(R->log_n1, R->log_n2, L * M, stream, B);
+  // transpose_kernel: reads limbs 0 .. L-1 of c0, writes L vectors of c0t
+  if (launch_recorder()) {
+    record_span("transpose: c0", ct, 0, (uint64_t)L * N * 8);
+    record_span("transpose: c0t", R->c0t, 0, (uint64_t)L * N * 8);
+  } else {
+    hipLaunchKernelGGL(fiona::transpose_kernel, dim3((N + 255) / 256, L), dim3(256), 0, stream, ct, R->c0t,
+                       R->log_n1, R->log_n2);
+  }
+
+  // 2. the inner products of every rotation (transposed layout, pi^-1 frame)
+  //    (batches of 8 digits, or of 4 where that pads fewer: L = 8, 16 take 8, L = 10, 12 take 4)
+  const dim3 ks_grid(M * (N / fiona::kKsTile));
+  const uint32_t round = fiona::ks_round(L);
+  const size_t ks_smem = fiona::ks_lds_bytes(L, round);
+  const uint32_t pad8 = (L + 7) / 8 * 8 - L, pad4 = (L + 3) / 4 * 4 - L;
+  // ks_inner_kernel: digits (j < L, m < M, 16 bytes per lane pair), keys of
+  // rotations r < n_rot (digit j, polynomial p, modulus m), u' of every
+  // rotation, the limb constants of every modulus
+  const uint64_t key_words = (uint64_t)L * 2 * M * N;
+  if (launch_recorder()) {
+    record_span("ks_inner: Dhat", R->Dhat, 0, (uint64_t)L * M * N * 8);
+    record_span("ks_inner: keys", keys, 0, (uint64_t)n_rot * key_words * 8);
+    record_span("ks_inner: U", R->U, 0, (uint64_t)2 * n_rot * M * N * 8);
+    record_span("ks_inner: limbs", R->limbs, 0, (uint64_t)M * sizeof(fiona::LimbConst));
+  } else if (pad8 <= pad4) {
+    hipLaunchKernelGGL(fiona::ks_inner_kernel<8>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat, keys,
+                       R->U, R->limbs, N, L, n_rot, round);
+  } else {
+    hipLaunchKernelGGL(fiona::ks_inner_kernel<4>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat,
+                       keys, R->U, R->limbs, N, L, n_rot, round);
+  }
+
+  // 3. the division by P: u'_P back to centred coefficients (W), then per
+  //    data limb its transform, the subtraction from u', the product with
+  //    P^-1, c0 for the first polynomials and the automorphism, written to out
+  const uint32_t V = 2 * n_rot;
+  NttPass C{};
+  C.sets = R->p_inv_set;
+  C.vps = V;
+  C.log_n1 = R->log_n1;
+  C.log_n2 = R->log_n2;
+  C.in = R->U + (size_t)L * N;
+  C.in_end = R->U_end;
+  C.in_stride = (size_t)M * N;
+  C.tmp = R->T;
+  C.tmp_end = R->T_end;
+  C.out = R->W;
+  C.out_end = R->W_end;
+  C.out_stride = N;
+  C.load = fiona::kLoadU64T;
+  C.store = fiona::kStoreF64;
+  launch_transform(R->log_n1, R->log_n2, V, stream, C);
+  NttPass Q{};
+  Q.sets = R->down_sets;
+  Q.vps = V;
+  Q.log_n1 = R->log_n1;
+  Q.log_n2 = R->log_n2;
+  Q.in = R->W;
+  Q.in_end = R->W_end;
+  Q.in_stride = N;
+  Q.tmp = R->T;
+  Q.tmp_end = R->T_end;
+  Q.out = out_cts;
+  Q.out_end = out_end;
+  Q.base = R->U;
+  Q.base_end = R->U_end;
+  Q.base_stride = (size_t)M * N;
+  Q.base_set_stride = N;
+  Q.add = R->c0t;
+  Q.add_end = R->c0t_end;
+  Q.add_set_stride = N;
+  Q.load = fiona::kLoadF64;
+  const uint32_t col_blocks = (1u << R->log_n1) / fiona::kNttCols;
+  Q.nsets_shared = L > 1 && (col_blocks * V) % 8 == 0 ? L : 0;
+  launch_pass(true, R->log_n2, R->log_n1, L * V, stream, Q);
+  fiona::RotArgs G{};
+  for (uint32_t r = 0; r < n_rot; ++r) G.g[r] = galois[r];
+  G.n_rot = n_rot;
+  G.L = L;
+  launch_rot_pass_b(R->log_n1, R->log_n2, L * V, stream, Q, G);
+}
+
+}  // namespace
+
+namespace fiona_host {
+
+// A rotator laid out at fake device addresses, one call with n_rot
+// rotations recorded (Galois elements 5^r mod 2N for r = 1 .. n_rot - 2,
+// then the conjugation 2N - 1 and the identity 1) and every access of its
+// launches checked; the output region is out_shrink bytes short.
+int rotate_replay(const uint64_t *moduli, uint32_t N, uint32_t L, uint32_t max_rot, uint32_t n_rot,
+                  uint64_t out_shrink, std::string &err) {
+  fiona_ctx *ctx = nullptr;
+  int rc = fiona_ctx_create(N, L, moduli, &ctx);
+  if (rc != FIONA_OK) return rc;
+  fiona_rotator R;
+  TableImage img;
+  size_t total = 0;
+  rc = rotator_layout(ctx, moduli[L], nullptr, max_rot, &R, img, total);
+  if (rc == FIONA_OK && (n_rot == 0 || n_rot > max_rot)) rc = FIONA_ERR_ARG;
   if (rc != FIONA_OK) {
-    fiona_rotator_destroy(R);
+    fiona_ctx_destroy(R.ext);
+    fiona_ctx_destroy(ctx);
     return rc;
   }
+  std::vector<uint32_t> galois(n_rot);
+  uint64_t g = 1;
+  for (uint32_t r = 0; r < n_rot; ++r) {
+    g = g * 5 % (2ull * N);
+    galois[r] = (uint32_t)g;
+  }
+  if (n_rot >= 2) galois[n_rot - 2] = 2 * N - 1;
+  galois[n_rot - 1] = 1;
+  // (each starts with bit 31 of its low address half set: the replay
+  // rebuilds every descriptor base from its halves as the kernels do)
+  const uint64_t kGap = 1ull << 44, kLow = 0x80000000ull;
+  char *dev = (char *)(uintptr_t)(1 * kGap + kLow);
+  const uint64_t *ct = (const uint64_t *)(uintptr_t)(2 * kGap + kLow);
+  const uint64_t *keys = (const uint64_t *)(uintptr_t)(3 * kGap + kLow);
+  uint64_t *out = (uint64_t *)(uintptr_t)(4 * kGap + kLow);
+  rotator_place(&R, img, dev);
+  std::vector<Region> regions = table_regions(img, dev);
+  regions.push_back(Region{(uint64_t)R.limbs, (uint64_t)R.limbs + (L + 1) * sizeof(fiona::LimbConst), "limbs"});
+  regions.push_back(Region{(uint64_t)R.D, (uint64_t)R.D_end, "D"});
+  regions.push_back(Region{(uint64_t)R.Dhat, (uint64_t)R.Dhat_end, "Dhat"});
+  regions.push_back(Region{(uint64_t)R.c0t, (uint64_t)R.c0t_end, "c0t"});
+  regions.push_back(Region{(uint64_t)R.T, (uint64_t)R.T_end, "T"});
+  regions.push_back(Region{(uint64_t)R.W, (uint64_t)R.W_end, "W"});
+  regions.push_back(Region{(uint64_t)R.U, (uint64_t)R.U_end, "U"});
+  regions.push_back(Region{(uint64_t)ct, (uint64_t)(ct + (size_t)2 * L * N), "ct"});
+  regions.push_back(Region{(uint64_t)keys, (uint64_t)(keys + (size_t)n_rot * fiona_rotation_key_words(&R)), "keys"});
+  regions.push_back(Region{(uint64_t)out, (uint64_t)(out + (size_t)n_rot * 2 * L * N) - out_shrink, "out_cts"});
+  LaunchRecord rec;
+  launch_recorder() = &rec;
+  rotate_enqueue(&R, ct, n_rot, galois.data(), keys, out, nullptr);
+  launch_recorder() = nullptr;
+  err = check_launches(rec, regions, (uint64_t)img.sets_addr(dev), img.sets_at(dev));
+  fiona_ctx_destroy(R.ext);
+  fiona_ctx_destroy(ctx);
+  return err.empty() ? FIONA_OK : FIONA_ERR_BOUNDS;
+}
+
+}  // namespace fiona_host
+
+extern "C" {
+
+int fiona_rotator_create(const fiona_ctx *ctx, uint64_t special_prime, const uint64_t *psi, uint32_t max_rot,
+                         fiona_rotator **out) {
+  if (!out) return FIONA_ERR_ARG;
+  *out = nullptr;
+  if (!ctx) return FIONA_ERR_ARG;
+  fiona_rotator *R = new (std::nothrow) fiona_rotator;
+  if (!R) return FIONA_ERR_NOMEM;
   try {
     TableImage img;
-    for (uint32_t j = 0; j < L; ++j) img.add(make_tables(R->log_n1, R->log_n2, mods[j], roots[j], true), mods[j]);
-    for (uint32_t i = 0; i <= L; ++i) img.add(make_tables(R->log_n1, R->log_n2, mods[i], roots[i], false), mods[i]);
-    for (uint32_t l = 0; l < L; ++l)
-      img.add(make_tables(R->log_n1, R->log_n2, mods[l], roots[l], false), mods[l],
-              make_tw(powmod_h(P % mods[l], mods[l] - 2, mods[l]), mods[l]));
-    img.add(make_tables(R->log_n1, R->log_n2, P, roots[L], true), P);
-    const size_t img_bytes = img.bytes();
-    const size_t limb_bytes = round256((L + 1) * sizeof(fiona::LimbConst));
-    const size_t vec = (size_t)N * 8;
-    const size_t d_bytes = round256(L * vec);
-    const size_t dhat_bytes = round256((size_t)L * (L + 1) * vec);
-    const size_t c0_bytes = round256(L * vec);
-    const size_t t_vectors = std::max((size_t)L * (L + 1), (size_t)2 * L * max_rot);
-    const size_t t_bytes = round256(t_vectors * vec);
-    const size_t w_bytes = round256((size_t)2 * max_rot * vec);
-    const size_t u_bytes = round256((size_t)max_rot * 2 * (L + 1) * vec);
+    size_t total = 0;
+    const int rc = rotator_layout(ctx, special_prime, psi, max_rot, R, img, total);
+    if (rc != FIONA_OK) {
+      fiona_rotator_destroy(R);
+      return rc;
+    }
     if (hipGetDevice(&R->device) != hipSuccess) {
       fiona_rotator_destroy(R);
       return FIONA_ERR_HIP;
     }
-    const size_t total = img_bytes + limb_bytes + d_bytes + dhat_bytes + c0_bytes + t_bytes + w_bytes + u_bytes;
-    if (hipMalloc(&R->dev, total) != hipSuccess) {
-      R->dev = nullptr;
+    void *dev = nullptr;
+    if (hipMalloc(&dev, total) != hipSuccess) {
       fiona_rotator_destroy(R);
       return FIONA_ERR_NOMEM;
     }
-    const NttSet *sets = img.upload(R->dev);
-    char *p = (char *)R->dev + img_bytes;
-    if (!sets || hipMemcpy(p, R->ext->limbs.data(), (L + 1) * sizeof(fiona::LimbConst), hipMemcpyHostToDevice) !=
-                     hipSuccess) {
+    rotator_place(R, img, dev);
+    if (!img.upload(R->dev) || hipMemcpy((void *)R->limbs, R->ext->limbs.data(),
+                                         (R->L + 1) * sizeof(fiona::LimbConst), hipMemcpyHostToDevice) != hipSuccess) {
       fiona_rotator_destroy(R);
       return FIONA_ERR_HIP;
     }
-    R->inv_sets = sets;
-    R->fwd_sets = sets + L;
-    R->down_sets = sets + 2 * L + 1;
-    R->p_inv_set = sets + 3 * L + 1;
-    R->limbs = (const fiona::LimbConst *)p;
-    p += limb_bytes;
-    R->D = (uint64_t *)p;
-    p += d_bytes;
-    R->Dhat = (uint64_t *)p;
-    p += dhat_bytes;
-    R->c0t = (uint64_t *)p;
-    p += c0_bytes;
-    R->T = (double *)p;
-    p += t_bytes;
-    R->W = (double *)p;
-    p += w_bytes;
-    R->U = (uint64_t *)p;
-    const int ks_smem = (int)fiona::ks_lds_bytes(L, fiona::ks_round(L));
+    const int ks_smem = (int)fiona::ks_lds_bytes(R->L, fiona::ks_round(R->L));
     const int nt_smem = (int)(fiona::kNttCols * fiona::padded_len(fiona::kNttMaxSide) * sizeof(double) +
                               fiona::kNttMaxSide / 2 * sizeof(Tw));
-    if (!allow_smem() ||
-        hipFuncSetAttribute((const void *)fiona::ntt_pass_b_rot<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            nt_smem) != hipSuccess ||
-        !allow_rot_smem(nt_smem) ||
+    if (!allow_smem() || !allow_rot_smem(nt_smem) ||
         hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             ks_smem) != hipSuccess ||
         hipFuncSetAttribute((const void *)fiona::ks_inner_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -471,95 +680,7 @@ int fiona_hoisted_rotate(const fiona_rotator *R, const uint64_t *ct, uint32_t n_
     return FIONA_ERR_ALIAS;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != R->device) return FIONA_ERR_ARG;
-  const uint32_t M = L + 1;
-
-  // 1. digits of c1, once: D_j = INTT_{q_j}(c1_j), then Dhat[j][m] = NTT_m(D_j)
-  //    (transposed layout); c0 transposed for step 3
-  NttPass A{};
-  A.sets = R->inv_sets;
-  A.vps = 1;
-  A.log_n1 = R->log_n1;
-  A.log_n2 = R->log_n2;
-  A.in = ct + (size_t)L * N;
-  A.in_set_stride = N;
-  A.tmp = R->T;
-  A.out = R->D;
-  A.out_set_stride = N;
-  A.load = fiona::kLoadU64;
-  A.store = fiona::kStoreU64;
-  launch_transform(R->log_n1, R->log_n2, L, stream, A);
-  NttPass B{};
-  B.sets = R->fwd_sets;
-  B.vps = L;
-  B.log_n1 = R->log_n1;
-  B.log_n2 = R->log_n2;
-  B.in = R->D;
-  B.in_stride = N;
-  B.tmp = R->T;
-  B.out = R->Dhat;
-  B.out_stride = (size_t)M * N;
-  B.out_set_stride = N;
-  B.load = fiona::kLoadU64;
-  B.store = fiona::kStoreU64;
-  B.out_transposed = 1;
-  B.nsets_shared = ((1u << R->log_n1) / fiona::kNttCols * L) % 8 == 0 ? M : 0;   // every modulus reads D_j
-  launch_transform(R->log_n1, R->log_n2, L * M, stream, B);
-  hipLaunchKernelGGL(fiona::transpose_kernel, dim3((N + 255) / 256, L), dim3(256), 0, stream, ct, R->c0t, R->log_n1,
-                     R->log_n2);
-
-  // 2. the inner products of every rotation (transposed layout, pi^-1 frame)
-  //    (batches of 8 digits, or of 4 where that pads fewer: L = 8, 16 take 8, L = 10, 12 take 4)
-  const dim3 ks_grid(M * (N / fiona::kKsTile));
-  const uint32_t round = fiona::ks_round(L);
-  const size_t ks_smem = fiona::ks_lds_bytes(L, round);
-  const uint32_t pad8 = (L + 7) / 8 * 8 - L, pad4 = (L + 3) / 4 * 4 - L;
-  if (pad8 <= pad4)
-    hipLaunchKernelGGL(fiona::ks_inner_kernel<8>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat, keys,
-                       R->U, R->limbs, N, L, n_rot, round);
-  else
-    hipLaunchKernelGGL(fiona::ks_inner_kernel<4>, ks_grid, dim3(fiona::kKsWaves * 64), ks_smem, stream, R->Dhat,
-                       keys, R->U, R->limbs, N, L, n_rot, round);
-
-  // 3. the division by P: u'_P back to centred coefficients (W), then per
-  //    data limb its transform, the subtraction from u', the product with
-  //    P^-1, c0 for the first polynomials and the automorphism, written to out
-  const uint32_t V = 2 * n_rot;
-  NttPass C{};
-  C.sets = R->p_inv_set;
-  C.vps = V;
-  C.log_n1 = R->log_n1;
-  C.log_n2 = R->log_n2;
-  C.in = R->U + (size_t)L * N;
-  C.in_stride = (size_t)M * N;
-  C.tmp = R->T;
-  C.out = R->W;
-  C.out_stride = N;
-  C.load = fiona::kLoadU64T;
-  C.store = fiona::kStoreF64;
-  launch_transform(R->log_n1, R->log_n2, V, stream, C);
-  NttPass Q{};
-  Q.sets = R->down_sets;
-  Q.vps = V;
-  Q.log_n1 = R->log_n1;
-  Q.log_n2 = R->log_n2;
-  Q.in = R->W;
-  Q.in_stride = N;
-  Q.tmp = R->T;
-  Q.out = out_cts;
-  Q.base = R->U;
-  Q.base_stride = (size_t)M * N;
-  Q.base_set_stride = N;
-  Q.add = R->c0t;
-  Q.add_set_stride = N;
-  Q.load = fiona::kLoadF64;
-  const uint32_t col_blocks = (1u << R->log_n1) / fiona::kNttCols;
-  Q.nsets_shared = L > 1 && (col_blocks * V) % 8 == 0 ? L : 0;
-  launch_pass(true, R->log_n2, R->log_n1, L * V, stream, Q);
-  fiona::RotArgs G{};
-  for (uint32_t r = 0; r < n_rot; ++r) G.g[r] = galois[r];
-  G.n_rot = n_rot;
-  G.L = L;
-  launch_rot_pass_b(R->log_n1, R->log_n2, L * V, stream, Q, G);
+  rotate_enqueue(R, ct, n_rot, galois, keys, out_cts, stream);
   return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
 }
 

@@ -43,7 +43,7 @@ def test_synth_library_exports():
 
 def test_status_strings():
     L = fiona.lib()
-    for code in range(-8, 1):
+    for code in range(-10, 1):
         assert L.fiona_status_string(code)
     assert L.fiona_status_string(0) == b"ok"
 
@@ -322,3 +322,24 @@ def test_rescaler_size_limit():
     with pytest.raises(fiona.FionaError) as e:
         fiona.Rescaler(ctx, 40000)
     assert e.value.status == -3
+
+
+def test_partial_sharing_with_repeated_inputs():
+    """A group may name the same input twice (a diagonal group wider than the
+    baby steps).  Pairs of one input with itself are no sharing candidates,
+    and taking a pair out of a sum removes exactly its two members: 32 groups
+    {A0, A0, Ak, Ak+1} keep their 4 members each (3 Add/Sub per sum)."""
+    q = synth.ntt_primes(16, 1)
+    ctx = fiona.Ctx(16, 1, q)
+    n_out = 32
+    mem_in, gm = [], [0]
+    for k in range(1, n_out + 1):
+        mem_in += [0, 0, k, k + 1]
+        gm.append(len(mem_in))
+    args = dict(n_in=n_out + 2, n_out=n_out, n_pt=0, n_scale=n_out, pm_off=[0] * (n_out + 1), pm_input=[],
+                pm_pt=[], grp_off=list(range(n_out + 1)), grp_mem_off=gm, mem_input=mem_in,
+                mem_sign=[1] * len(mem_in), grp_scale=list(range(n_out)))
+    st = fiona.Plan(ctx, flags=HOST | fiona.FIONA_PLAN_NO_LDS_SUMS, **args).stats()
+    assert st["n_member_nonzero"] == 4 * n_out
+    assert st["addsub_shared"] == 3 * n_out
+    assert st["n_partial"] == 0 and st["addsub_partial"] == 3 * n_out

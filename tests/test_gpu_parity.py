@@ -104,6 +104,10 @@ SMALL = {
     "all_ternary": synth.LayerConfig("all_ternary", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=1.0, pool=3),
     "all_raw": synth.LayerConfig("all_raw", N=320, L=2, n_in=12, n_out=5, T=24, g=6, ternary=0.0),
     "partial_share": synth.LayerConfig("partial_share", N=256, L=2, n_in=16, n_out=48, T=96, g=12, ternary=0.95),
+    # groups wider than the inputs: a group names an input more than once
+    "repeated_pool": synth.LayerConfig("repeated_pool", N=256, L=2, n_in=6, n_out=48, T=80, g=10, ternary=0.9,
+                                       pool=4),
+    "repeated_iid": synth.LayerConfig("repeated_iid", N=256, L=2, n_in=7, n_out=48, T=160, g=20, ternary=0.9),
 }
 
 
@@ -154,7 +158,9 @@ def test_small_layer_elementwise(dev, name):
                                         ("partial_share", fiona.FIONA_PLAN_PER_CONTRIBUTION),
                                         ("many_outputs", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
                                         ("partial_share", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
-                                        ("fold_raw", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS)])
+                                        ("fold_raw", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
+                                        ("repeated_pool", fiona.FIONA_PLAN_NO_LDS_SUMS),
+                                        ("repeated_pool", fiona.FIONA_PLAN_NO_PARTIAL_SHARING)])
 def test_plan_variants_agree(dev, name, flags):
     layer = _small_layer(name)
     x, pt = synth.input_values(layer), synth.pt_values(layer)
@@ -325,7 +331,7 @@ def test_full_size_sampled(dev, name):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("name,width", [("vgg11", 2048), ("bert_ffn", 1024)])
+@pytest.mark.parametrize("name,width", [("vgg11", 2048), ("vit768", 2048), ("bert_ffn", 1024)])
 def test_full_size_contiguous_tiles(dev, name, width):
     """Full-size layer in the benchmark's launch configuration: every output at
     every coefficient of a run of whole tiles at the start of limb 0 and at the
@@ -417,3 +423,121 @@ def test_runtime_signs_are_read(dev):
     expect = oracle.weighted_sum_layer(lay2, x, pt)
     out_t, *_ = _run(layer, dev, x, pt, flags=fiona.FIONA_PLAN_NO_SHARING, signs=signs2)
     _assert_equal(_host(out_t, layer), expect, "run-time signs")
+
+
+# ---------------------------------------------------------------------------
+# Route equivalence at full size (Sec. 3 Obs. 2 / Table 1: the hybrid and the
+# all-PMult forms of a layer compute the same outputs), every output chunk
+# ---------------------------------------------------------------------------
+
+def _run_all_chunks(layer, dev, in_t, n_chunks, tag):
+    """Every output chunk of `layer` in the benchmark's launch configuration
+    (padded plaintext rows, one plaintext buffer refilled per chunk); returns
+    the full [n_out][2][L][N] output on the device and the chunk ranges."""
+    import torch
+    import synth.gpu
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    pitch = ctx.pt_pitch_hint()
+    chunks = synth.output_chunks(layer.n_out, n_chunks)
+    subs = [synth.chunk_layer(layer, a, b) for a, b in chunks]
+    LN = layer.L * layer.N
+    pt_t = torch.empty((max(max(1, s.n_pt) for s in subs) - 1) * pitch + LN, dtype=torch.int64, device=dev)
+    out = torch.full((layer.n_out * 2 * LN,), -1, dtype=torch.int64, device=dev)
+    for ci, ((a, b), sub) in enumerate(zip(chunks, subs)):
+        synth.gpu.fill_pts(sub, pt_t, pitch)
+        plan = fiona.Plan.from_layer(ctx, sub, pt_pitch=pitch)
+        sign_t = _to_dev(sub.mem_sign, np.int8, dev) if sub.mem_sign.size else \
+            torch.zeros(1, dtype=torch.int8, device=dev)
+        scale_t = _to_dev(sub.scales, np.int64, dev) if sub.scales.size else \
+            torch.zeros(1, dtype=torch.int64, device=dev)
+        fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out[a * 2 * LN: b * 2 * LN])
+        torch.cuda.synchronize()
+        if ci % 8 == 0 or ci == len(chunks) - 1:
+            _say("[parity] %s chunk %d/%d (outputs %d..%d) done" % (tag, ci + 1, len(chunks), a, b - 1))
+        del plan
+    del pt_t
+    torch.cuda.empty_cache()
+    return out, chunks
+
+
+@pytest.mark.parametrize("name", ["vit768", "bert_ffn", "large4096"])
+def test_full_size_all_pmult_every_chunk(dev, name):
+    """The all-PMult layer (every signed term a PMult by its constant
+    plaintext h*c), run in the benchmark's output chunks, equals the hybrid
+    layer at every output, polynomial, limb and coefficient; each all-PMult
+    chunk also matches the oracle at sampled positions."""
+    import torch
+    import synth.gpu
+    layer = synth.make_layer(synth.CONFIGS[name], 1)
+    in_t = torch.empty(layer.n_in * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    synth.gpu.fill_inputs(layer, in_t)
+    out_h, _ = _run_all_chunks(layer, dev, in_t, layer.cfg.chunks_hybrid, name + " hybrid")
+    allpm = synth.all_pmult_layer(layer)
+    out_a, chunks = _run_all_chunks(allpm, dev, in_t, layer.cfg.chunks_allpm, name + " all-PMult")
+    LN = layer.L * layer.N
+    for ci, (a, b) in enumerate(chunks):
+        if not torch.equal(out_h[a * 2 * LN: b * 2 * LN], out_a[a * 2 * LN: b * 2 * LN]):
+            diff = (out_h[a * 2 * LN: b * 2 * LN] != out_a[a * 2 * LN: b * 2 * LN]).nonzero()
+            w = int(diff[0]) + a * 2 * LN
+            raise AssertionError("%s all-PMult chunk %d differs from hybrid at %d words; first at out %d poly %d "
+                                 "limb %d coeff %d" % (name, ci, diff.numel(), w // (2 * LN), (w // LN) % 2,
+                                                       (w // layer.N) % layer.L, w % layer.N))
+    _say("[parity] %s: all-PMult == hybrid at all %d outputs x 2 x %d x %d" % (name, layer.n_out, layer.L, layer.N))
+    limbs, coeffs = synth.sample_positions(layer.N, layer.L, 10, 103)
+    x_s = synth.input_values(layer, (limbs, coeffs))
+    for ci, (a, b) in enumerate(chunks):
+        sub = synth.chunk_layer(allpm, a, b)
+        expect = oracle.weighted_sum_sampled(sub, limbs, coeffs, x_s, synth.pt_values(sub, (limbs, coeffs)),
+                                             n_threads=16)
+        got = out_a[a * 2 * LN: b * 2 * LN].view(b - a, 2, layer.L, layer.N)[:, :, limbs, coeffs]
+        got = got.cpu().numpy().view(np.uint64)
+        bad = np.argwhere(got != expect)
+        if bad.size:
+            j, p, s = (int(v) for v in bad[0])
+            raise AssertionError("%s all-PMult chunk %d: %d mismatches with the oracle; first at out %d poly %d "
+                                 "limb %d coeff %d" % (name, ci, len(bad), a + j, p, limbs[s], coeffs[s]))
+    del out_h, out_a, in_t
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged_pool", "partial_share", "repeated_pool"])
+def test_small_all_pmult_elementwise(dev, name):
+    """The all-PMult form of a small layer on the GPU, element by element
+    against the oracle, and equal to the hybrid form's oracle result."""
+    layer = _small_layer(name)
+    allpm = synth.all_pmult_layer(layer)
+    x = synth.input_values(layer)
+    expect = oracle.weighted_sum_layer(allpm, x, synth.pt_values(allpm), n_threads=8)
+    _assert_equal(expect, oracle.weighted_sum_layer(layer, x, synth.pt_values(layer), n_threads=8),
+                  name + " oracle: all-PMult vs hybrid")
+    out_t, *_ = _run(allpm, dev, x, synth.pt_values(allpm))
+    _assert_equal(_host(out_t, allpm), expect, name + " all-PMult")
+
+
+@pytest.mark.parametrize("chunk", [0, 15])
+def test_full_size_large_contiguous_tiles(dev, chunk):
+    """Large 4096x4096 layer, one output chunk in the benchmark's launch
+    configuration: every output of the chunk at every coefficient of 16 whole
+    tiles at the start of limb 0 and 16 at the end of the last limb."""
+    import torch
+    import synth.gpu
+    layer = synth.make_layer(synth.CONFIGS["large4096"], 1)
+    a, b = synth.output_chunks(layer.n_out, layer.cfg.chunks_hybrid)[chunk]
+    sub = synth.chunk_layer(layer, a, b)
+    _say("[parity] large4096 chunk %d (outputs %d..%d): contiguous tiles" % (chunk, a, b - 1))
+    out_t, in_t, pt_t, plan = _run(sub, dev, pitch="hint")
+    del pt_t
+    L, N, width = layer.L, layer.N, 1024
+    limbs = np.concatenate([np.zeros(width, np.int64), np.full(width, L - 1, np.int64)])
+    coeffs = np.concatenate([np.arange(width), np.arange(N - width, N)]).astype(np.int64)
+    x_s = synth.input_values(sub, (limbs, coeffs))
+    expect = oracle.weighted_sum_sampled(sub, limbs, coeffs, x_s, synth.pt_values(sub, (limbs, coeffs)),
+                                         n_threads=16)
+    got = out_t[: sub.n_out * 2 * L * N].view(sub.n_out, 2, L, N)[:, :, limbs, coeffs].cpu().numpy().view(np.uint64)
+    bad = np.argwhere(got != expect)
+    if bad.size:
+        j, p, i = (int(v) for v in bad[0])
+        raise AssertionError("large4096 chunk %d: %d mismatches; first at out %d poly %d limb %d coeff %d"
+                             % (chunk, len(bad), a + j, p, limbs[i], coeffs[i]))
+    del out_t, in_t
+    torch.cuda.empty_cache()
