@@ -1,15 +1,26 @@
 """Benchmark of the hybrid weighted sum on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config vgg11] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--rounds R] [--layers vgg11,vit768,bert_ffn,large4096]
+                    [--no-cpu-baseline] [--ablation] [--rescale] [--rotate] [--config NAME]
 
-A step is one fiona_hybrid_linear call over the whole layer (every output,
-both polynomials, every limb and coefficient), inputs already resident in HBM.
-The default workload is the VGG11-like 3x3 conv layer (N=2^16, L=8, 64 input
-ciphertexts, 128 outputs x 64 terms, 53% ternary in groups of 8).  The same
-layer is also timed with every term as a PMult (all-PMult), which computes the
-identical outputs, for the speedup of the hybrid route.  Layers whose
-plaintext table exceeds the per-chunk budget run in output chunks (plaintexts
-regenerated on the device between chunks, untimed) and the chunk times add up.
+The metric is quoted on the four N=2^16 layers, so a default run times all
+four, each both ways: the hybrid layer (PMult for raw terms, Add/Sub and one
+scalar product per signed sum) and the same layer with every term a PMult
+(all-PMult), which computes identical outputs.  The two forms of a layer run
+on the same device buffers (one input, plaintext and output allocation per
+layer), alternating over R rounds.  Layers whose plaintext table exceeds the
+per-chunk budget run in output chunks: the chunk's plaintexts are generated
+on the device (untimed), then W untimed and K timed launches follow, one HIP
+event between consecutive launches on the kernels' stream.  A layer's step
+time is the sum over its chunks of the median launch time (over the K launches
+of every round); the mean, minimum and maximum are reported beside it.
+
+The headline record is the largest layer, the 4096x4096 one (16 output chunks
+of 8 outputs; each chunk's 77 GiB of plaintexts resident when its launches
+run).  Every layer carries its own roofline (algorithmic bytes per launch over
+the mean launch time, against 8 TB/s), counter traffic where the committed
+counter records match the kernel source, and the hybrid-vs-all-PMult speedup.
+Measured read and copy ceilings of the HBM sit beside the 8 TB/s spec.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -29,6 +40,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, vendor peak
 PROFILE_DIR = os.path.join(ROOT, "profiles")
+LAYERS = ("vgg11", "vit768", "bert_ffn", "large4096")
+METRIC = "ct-terms/sec and achieved HBM GB/s (hybrid vs all-PMult), N=2^16 layers, 1 GPU"
 
 
 def log(msg):
@@ -65,7 +78,7 @@ def kernel_source_hash() -> str:
     counter records name: a change of code makes them stale, a change of
     comments does not."""
     h = hashlib.sha256()
-    for name in ("fiona.hip", "hybrid_kernel.hpp", "modarith.hpp"):
+    for name in ("fiona.hip", "hybrid_kernel.hpp", "modarith.hpp", "buffer.hpp"):
         with open(os.path.join(ROOT, "paper_2609_35352_amd", "csrc", name), encoding="utf-8") as f:
             h.update(strip_comments(f.read()).encode())
     return h.hexdigest()[:16]
@@ -85,80 +98,99 @@ def measured_traffic(workload: str, variant: str):
     return None if v is None else float(v["bytes_per_launch"])
 
 
-def time_layer(layer, dev, steps, warmup, stream, label, flags=0, padded=True):
-    """Run every output chunk of `layer` with plans made under `flags`; return
-    (sum of per-chunk ms per launch, algorithmic bytes, per-chunk records).
-    time_layer.kernels names the kernel instances and time_layer.counts sums
-    the plans' operation counts over the chunks."""
+def _dev_signs_scales(sub, dev):
+    import torch
+    sign_t = torch.from_numpy(np.ascontiguousarray(sub.mem_sign)).to(dev) if sub.mem_sign.size else \
+        torch.zeros(1, dtype=torch.int8, device=dev)
+    scale_t = torch.from_numpy(np.ascontiguousarray(sub.scales.view(np.int64))).to(dev) if sub.scales.size \
+        else torch.zeros(1, dtype=torch.int64, device=dev)
+    return sign_t, scale_t
+
+
+def _pitch(ctx, layer, padded):
+    if padded is True:
+        return ctx.pt_pitch_hint()
+    if padded is False:
+        return layer.L * layer.N
+    return layer.L * layer.N + int(padded)
+
+
+def time_layer(name, dev, stream, steps, warmup, rounds, seed=1, padded=True):
+    """Both forms of one layer on the same buffers; returns the layer record."""
     import torch
     import synth
     import synth.gpu
     import paper_2609_35352_amd as fiona
 
-    cfg = layer.cfg
-    n_chunks = cfg.chunks_hybrid if layer.pt_const is None else cfg.chunks_allpm
-    chunks = synth.output_chunks(layer.n_out, n_chunks)
+    cfg = synth.CONFIGS[name]
+    layer = synth.make_layer(cfg, seed)
+    forms = {"hybrid": (layer, cfg.chunks_hybrid), "all_pmult": (synth.all_pmult_layer(layer), cfg.chunks_allpm)}
     ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
-    in_t = torch.empty(layer.n_in * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
+    pitch = _pitch(ctx, layer, padded)
+    LN = layer.L * layer.N
+    subs = {f: [synth.chunk_layer(lay, a, b) for a, b in synth.output_chunks(lay.n_out, nc)]
+            for f, (lay, nc) in forms.items()}
+    max_pt = max(max(1, s.n_pt) for ss in subs.values() for s in ss)
+    max_out = max(s.n_out for ss in subs.values() for s in ss)
+    in_t = torch.empty(layer.n_in * 2 * LN, dtype=torch.int64, device=dev)
     synth.gpu.fill_inputs(layer, in_t)
-    subs = [synth.chunk_layer(layer, a, b) for a, b in chunks]
-    # plaintext rows at the library's padded pitch (or packed, pitch L*N)
-    if padded is True:
-        pitch = ctx.pt_pitch_hint()
-    elif padded is False:
-        pitch = layer.L * layer.N
-    else:   # an explicit pad in words
-        pitch = layer.L * layer.N + int(padded)
-    max_pt = max(max(1, s.n_pt) for s in subs)
-    max_out = max(s.n_out for s in subs)
-    pt_t = torch.empty((max_pt - 1) * pitch + layer.L * layer.N, dtype=torch.int64, device=dev)
-    out_t = torch.empty(max_out * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
-    total_ms = 0.0
-    total_bytes = 0
-    per_chunk = []
-    waves = set()
-    counts = {}
-    for ci, sub in enumerate(subs):
-        synth.gpu.fill_pts(sub, pt_t, pitch)
-        plan = fiona.Plan.from_layer(ctx, sub, flags=flags, pt_pitch=pitch)
-        sign_t = torch.from_numpy(np.ascontiguousarray(sub.mem_sign)).to(dev) if sub.mem_sign.size else \
-            torch.zeros(1, dtype=torch.int8, device=dev)
-        scale_t = torch.from_numpy(np.ascontiguousarray(sub.scales.view(np.int64))).to(dev) if sub.scales.size \
-            else torch.zeros(1, dtype=torch.int64, device=dev)
-        torch.cuda.synchronize()
-        for _ in range(warmup):
-            fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
-        torch.cuda.synchronize()
-        # one event between consecutive launches: the mean over the steps and
-        # each launch's own time (min, median, max) from the same region
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-        ev[0].record(stream)
-        for i in range(steps):
-            fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
-            ev[i + 1].record(stream)
-        torch.cuda.synchronize()
-        ms = ev[0].elapsed_time(ev[steps]) / steps
-        each = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
-        nbytes = synth.algorithmic_bytes(sub)
-        total_ms += ms
-        total_bytes += nbytes
-        per_chunk.append({"outputs": sub.n_out, "ms": round(ms, 4), "alg_GBps": round(nbytes / ms / 1e6, 1),
-                          "ms_min": round(each[0], 4), "ms_median": round(float(np.median(each)), 4),
-                          "ms_max": round(each[-1], 4)})
-        st = plan.stats()
-        waves.add(st["waves"])
-        for key in ("pmult_grouped", "n_use", "addsub_partial", "n_partial", "n_sum_distinct"):
-            counts[key] = counts.get(key, 0) + st[key]
-        if ci == 0 or ci == len(subs) - 1 or ci % 8 == 0:
-            log("[bench] %s chunk %d/%d: %.3f ms/launch, %.1f GB/s algorithmic, plan %s"
-                % (label, ci + 1, len(subs), ms, nbytes / ms / 1e6, plan.stats()))
-        del plan
-    del pt_t, out_t, in_t
+    pt_t = torch.empty((max_pt - 1) * pitch + LN, dtype=torch.int64, device=dev)
+    out_t = torch.empty(max_out * 2 * LN, dtype=torch.int64, device=dev)
+    plans = {f: [fiona.Plan.from_layer(ctx, s, pt_pitch=pitch) for s in ss] for f, ss in subs.items()}
+    args = {f: [_dev_signs_scales(s, dev) for s in ss] for f, ss in subs.items()}
+    times = {f: [[] for _ in ss] for f, ss in subs.items()}
+    torch.cuda.synchronize()
+    for rd in range(rounds):
+        for f in forms:
+            for ci, sub in enumerate(subs[f]):
+                synth.gpu.fill_pts(sub, pt_t, pitch)   # untimed; synchronizes
+                plan, (sign_t, scale_t) = plans[f][ci], args[f][ci]
+                for _ in range(warmup):
+                    fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+                ev[0].record(stream)
+                for i in range(steps):
+                    fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
+                    ev[i + 1].record(stream)
+                torch.cuda.synchronize()
+                times[f][ci] += [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+            n = len(subs[f])
+            log("[bench] %s %s round %d/%d: %d chunk(s), %.3f ms (sum of this round's chunk medians)"
+                % (name, f, rd + 1, rounds, n, sum(float(np.median(t[-steps:])) for t in times[f])))
+    rec = {"layer": name, "description": cfg.description, "N": cfg.N, "L": cfg.L, "n_in": cfg.n_in,
+           "n_out": cfg.n_out, "terms_per_output": cfg.T, "group": cfg.g, "ct_terms": layer.ct_terms,
+           "pt_pitch_words": pitch, "pt_row_words": LN}
+    for f in forms:
+        t = times[f]
+        med = sum(float(np.median(x)) for x in t)
+        mean = sum(float(np.mean(x)) for x in t)
+        nbytes = sum(synth.algorithmic_bytes(s) for s in subs[f])
+        n = len(t)
+        st = [p.stats() for p in plans[f]]
+        waves = sorted({s["waves"] for s in st})
+        traffic = measured_traffic(name, "hybrid" if f == "hybrid" else "allpm")
+        rec[f] = {
+            "ms_per_step": round(med, 4), "ms_mean": round(mean, 4),
+            "ms_min": round(sum(min(x) for x in t), 4), "ms_max": round(sum(max(x) for x in t), 4),
+            "value": round(layer.ct_terms / (med * 1e-3), 1), "unit": "ct-terms/s",
+            "chunks": n, "timed_launches_per_chunk": len(t[0]),
+            "alg_bytes": nbytes, "alg_GBps": round(nbytes / med / 1e6, 1),
+            "roofline": {"bound": "hbm", "achieved": round(nbytes / mean / 1e6, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(nbytes / mean / 1e6 / HBM_PEAK_GBS, 4),
+                         "traffic": None if traffic is None else round(traffic),
+                         "alg_bytes_per_launch": nbytes // n,
+                         "kernel": " + ".join("hybrid_linear_kernel<%d>" % w for w in waves)},
+            "plan": {k: sum(s[k] for s in st) for k in ("n_pmult", "n_use", "n_sum_distinct", "addsub_partial",
+                                                         "n_partial")},
+        }
+        if n > 1:
+            rec[f]["chunk_ms_median"] = [round(float(np.median(x)), 4) for x in t]
+    rec["speedup_hybrid_vs_allpmult"] = round(rec["all_pmult"]["ms_per_step"] / rec["hybrid"]["ms_per_step"], 3)
+    rec["raw_words_per_s_hybrid"] = layer.n_pm * LN / (rec["hybrid"]["ms_per_step"] * 1e-3)
+    del plans, args, pt_t, out_t, in_t
+    torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    time_layer.kernels = ["hybrid_linear_kernel<%d>" % w for w in sorted(waves)]
-    time_layer.pitch = pitch
-    time_layer.counts = counts
-    return total_ms, total_bytes, per_chunk
+    return rec
 
 
 def time_plan_variants(layer, dev, steps, warmup, stream, variants, padded=True, rounds=3):
@@ -176,8 +208,7 @@ def time_plan_variants(layer, dev, steps, warmup, stream, variants, padded=True,
     cfg = layer.cfg
     chunks = synth.output_chunks(layer.n_out, cfg.chunks_hybrid if layer.pt_const is None else cfg.chunks_allpm)
     ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
-    pitch = ctx.pt_pitch_hint() if padded is True else (layer.L * layer.N if padded is False
-                                                        else layer.L * layer.N + int(padded))
+    pitch = _pitch(ctx, layer, padded)
     subs = [synth.chunk_layer(layer, a, b) for a, b in chunks]
     in_t = torch.empty(layer.n_in * 2 * layer.L * layer.N, dtype=torch.int64, device=dev)
     synth.gpu.fill_inputs(layer, in_t)
@@ -187,10 +218,7 @@ def time_plan_variants(layer, dev, steps, warmup, stream, variants, padded=True,
     res = {name: [0.0, {}] for name, _ in variants}
     for ci, sub in enumerate(subs):
         synth.gpu.fill_pts(sub, pt_t, pitch)
-        sign_t = torch.from_numpy(np.ascontiguousarray(sub.mem_sign)).to(dev) if sub.mem_sign.size else \
-            torch.zeros(1, dtype=torch.int8, device=dev)
-        scale_t = torch.from_numpy(np.ascontiguousarray(sub.scales.view(np.int64))).to(dev) if sub.scales.size \
-            else torch.zeros(1, dtype=torch.int64, device=dev)
+        sign_t, scale_t = _dev_signs_scales(sub, dev)
         plans = {name: fiona.Plan.from_layer(ctx, sub, flags=flags, pt_pitch=pitch) for name, flags in variants}
         best = {name: float("inf") for name, _ in variants}
         torch.cuda.synchronize()
@@ -296,32 +324,61 @@ def time_rescale(layer, dev, steps, warmup, stream):
     return {"ciphertexts": n, "ms": round(ms, 4), "ct_per_s": round(n / (ms * 1e-3), 1),
             "alg_bytes": nbytes, "alg_GBps": round(nbytes / ms / 1e6, 1),
             "frac_of_hbm_peak": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4),
-            "butterflies_per_s": round(butterflies / (ms * 1e-3), 1),
-            "launches": 2 * L}
+            "butterflies_per_s": round(butterflies / (ms * 1e-3), 1)}
 
 
-def cpu_baseline(layer, seconds: float = 10.0):
-    """The oracle (test infrastructure, plain C) on a bounded sample of the same layer."""
+def host_cpu():
+    """CPU model, the host's CPU count and the threads this process may use
+    (its affinity, capped by OMP_NUM_THREADS where set: a GPU machine gives one
+    GPU's job a share of its cores)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    cap = os.environ.get("OMP_NUM_THREADS")
+    threads = min(avail, int(cap)) if cap and cap.isdigit() and int(cap) > 0 else avail
+    return model, os.cpu_count() or 1, avail, threads
+
+
+def cpu_baseline(layer, seconds: float = 10.0, n_pos: int = None):
+    """The oracle (test infrastructure, plain C) on a bounded sample of the same
+    layer: n_pos (limb, coefficient) positions x every output and term, both
+    polynomials, chunk by chunk for a chunked layer, repeated for about
+    `seconds`; scaled to the whole layer.  By default n_pos keeps the sampled
+    plaintext values (generated in NumPy before timing) near 10^7."""
     import oracle
     import synth
 
-    threads = min(os.cpu_count() or 1, 16)
-    S = 2048
-    limbs, coeffs = synth.sample_positions(layer.N, layer.L, S, 7)
+    model, ncpu, avail, threads = host_cpu()
+    if n_pos is None:
+        n_pos = int(min(2048, max(16, 10_000_000 // max(1, layer.n_pt))))
+    limbs, coeffs = synth.sample_positions(layer.N, layer.L, max(0, n_pos - 6), 7)
     x_s = synth.input_values(layer, (limbs, coeffs))
-    pt_s = synth.pt_values(layer, (limbs, coeffs))
-    n_pos = len(limbs)
+    chunks = [synth.chunk_layer(layer, a, b) for a, b in synth.output_chunks(layer.n_out, layer.cfg.chunks_hybrid)]
+    pts = [synth.pt_values(c, (limbs, coeffs)) for c in chunks]
     passes, t = 0, 0.0
     while t < seconds and passes < 1000:
         t0 = time.perf_counter()
-        oracle.weighted_sum_sampled(layer, limbs, coeffs, x_s, pt_s, n_threads=threads)
+        for c, pt_s in zip(chunks, pts):
+            oracle.weighted_sum_sampled(c, limbs, coeffs, x_s, pt_s, n_threads=threads)
         t += time.perf_counter() - t0
         passes += 1
-    frac = n_pos / float(layer.L * layer.N)
+    frac = len(limbs) / float(layer.L * layer.N)
     value = layer.ct_terms * frac * passes / t
     return {"value": value, "unit": "ct-terms/s", "cores": threads, "kind": "oracle",
-            "sample": "%d (limb, coeff) positions of the layer x all %d outputs x %d terms x 2 polys, %d passes "
-                      "in %.1f s (inputs generated before timing)" % (n_pos, layer.n_out, layer.cfg.T, passes, t)}
+            "cpu_model": model, "host_cpus": ncpu, "cpus_available": avail,
+            "sample": "%d (limb, coeff) positions of %s x all %d outputs x %d terms x 2 polys, %d passes in %.1f s "
+                      "(per-term __int128 products and %%, inputs generated before timing); scaled by the positions' "
+                      "share of the layer" % (len(limbs), layer.cfg.name, layer.n_out, layer.cfg.T, passes, t)}
 
 
 def time_mac_microbench(stream, blocks=2048, chunks=200, reps=5):
@@ -345,16 +402,52 @@ def time_mac_microbench(stream, blocks=2048, chunks=200, reps=5):
             "threads": blocks * 256}
 
 
+def time_streams(stream, gib=4, reps=5):
+    """Measured HBM ceilings: a plain contiguous read and a plain copy of
+    `gib` GiB (best grid of four), next to the 8 TB/s spec."""
+    import torch
+    import paper_2609_35352_amd as fiona
+
+    n = (gib << 30) // 8
+    src = torch.ones(n, dtype=torch.int64, device="cuda:0")
+    dst = torch.empty_like(src)
+    sink = torch.empty(1 << 15, dtype=torch.int64, device="cuda:0")
+    out = {}
+    for kind in ("read", "copy"):
+        best = None
+        for blocks in (2048, 4096, 8192, 16384):
+            run = (lambda: fiona.stream_read(src, blocks, sink, stream=stream)) if kind == "read" else \
+                (lambda: fiona.stream_copy(src, dst, blocks, stream=stream))
+            nbytes = run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                run()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            gbs = nbytes / (e0.elapsed_time(e1) / reps) / 1e6
+            if best is None or gbs > best[0]:
+                best = (gbs, blocks)
+        out[kind] = {"GBps": round(best[0], 1), "frac_of_spec": round(best[0] / HBM_PEAK_GBS, 4),
+                     "workgroups": best[1], "bytes": n * 8 * (1 if kind == "read" else 2)}
+    del src, dst, sink
+    torch.cuda.empty_cache()
+    out["spec_GBps"] = HBM_PEAK_GBS
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="vgg11")
+    ap.add_argument("--rounds", type=int, default=2, help="rounds of hybrid then all-PMult per layer")
+    ap.add_argument("--layers", default=",".join(LAYERS), help="comma-separated layers to time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-allpmult", action="store_true", help="time only the hybrid layer")
-    ap.add_argument("--only-allpmult", action="store_true", help="time only the all-PMult layer")
+    ap.add_argument("--no-streams", action="store_true", help="skip the read and copy ceilings")
     ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--config", default="vgg11", help="the layer of --ablation, --rescale and --rotate")
     ap.add_argument("--rotate", action="store_true",
                     help="also time the hoisted baby-step rotations that produce the layer's inputs "
                          "(fiona_hoisted_rotate)")
@@ -395,113 +488,86 @@ def main():
     fiona.lib()
     dev = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=dev)   # default priority
-    cfg = synth.CONFIGS[args.config]
-    layer = synth.make_layer(cfg, args.seed)
     pad_mode = False if args.packed_pts else (True if args.pt_pad is None else args.pt_pad)
-    log("[bench] %s: %s" % (cfg.name, cfg.description))
+    names = [n for n in args.layers.split(",") if n]
+    for n in names:
+        if n not in synth.CONFIGS:
+            raise SystemExit("unknown layer %s" % n)
 
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
-    if args.only_allpmult:
-        apl = synth.all_pmult_layer(layer)
-        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult",
-                                                padded=pad_mode)
-        print(json.dumps({"variant": "all-PMult", "workload": cfg.name, "ms_per_step": round(ap_ms, 4),
-                          "value": round(layer.ct_terms / (ap_ms * 1e-3), 1), "unit": "ct-terms/s",
-                          "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "chunks": ap_chunks}), flush=True)
-        return
-    hy_ms, hy_bytes, hy_chunks = time_layer(layer, dev, args.steps, args.warmup, stream, "hybrid",
-                                            padded=pad_mode)
-    hy_kernels = time_layer.kernels
-    hy_pitch = time_layer.pitch
-    torch.cuda.synchronize()
-    hy_value = layer.ct_terms / (hy_ms * 1e-3)
-    hy_gbs = hy_bytes / hy_ms / 1e6
+    records = []
+    for n in names:
+        log("[bench] %s: %s" % (n, synth.CONFIGS[n].description))
+        records.append(time_layer(n, dev, stream, args.steps, args.warmup, args.rounds, args.seed, pad_mode))
+    head = next((r for r in records if r["layer"] == "large4096"), records[-1])
 
-    allpm = None
-    if not args.no_allpmult:
-        apl = synth.all_pmult_layer(layer)
-        ap_ms, ap_bytes, ap_chunks = time_layer(apl, dev, args.steps, args.warmup, stream, "all-PMult",
-                                                padded=pad_mode)
-        allpm = {"value": round(layer.ct_terms / (ap_ms * 1e-3), 1), "ms_per_step": round(ap_ms, 4),
-                 "alg_GBps": round(ap_bytes / ap_ms / 1e6, 1), "alg_bytes": ap_bytes,
-                 "frac_of_hbm_peak": round(ap_bytes / ap_ms / 1e6 / HBM_PEAK_GBS, 4),
-                 "chunks": len(ap_chunks), "speedup_hybrid_vs_allpmult": round(ap_ms / hy_ms, 3)}
-    ablation = None
-    if args.ablation:
-        # the compilations of Sec. 6.2 on the same kernel: every signed term's
-        # factor applied on its own, then grouping, then sharing whole sums,
-        # then sharing partly overlapping sums as well (the default plan)
-        # (all four on the same buffers, interleaved: see time_plan_variants)
-        ablation = []
-        variants = (("per-contribution", fiona.FIONA_PLAN_PER_CONTRIBUTION),
-                    ("+grouping", fiona.FIONA_PLAN_NO_SHARING),
-                    ("+sharing", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
-                    ("+partial sharing", 0))
-        timed = time_plan_variants(layer, dev, args.steps, args.warmup, stream, variants, padded=pad_mode)
-        for name, _ in variants:
-            ms, c = timed[name]
-            ablation.append({"plan": name, "ms_per_step": round(ms, 4),
-                             "value": round(layer.ct_terms / (ms * 1e-3), 1),
-                             "scalar_products": c["n_use"], "pmult": c["pmult_grouped"] - c["n_use"],
-                             "addsub": c["addsub_partial"], "common_terms": c["n_partial"],
-                             "speedup_vs_per_contribution": None})
-        for rec in ablation:
-            rec["speedup_vs_per_contribution"] = round(ablation[0]["ms_per_step"] / rec["ms_per_step"], 3)
-    rescale = None
-    if args.rescale:
-        rescale = time_rescale(layer, dev, args.steps, args.warmup, stream)
-    rotate = None
-    if args.rotate:
-        rotate = time_rotate(layer, dev, args.steps, args.warmup, stream)
-    # the hybrid launch's raw-term multiply-adds against the register-only rate
+    extra = {}
+    if args.ablation or args.rescale or args.rotate:
+        layer = synth.make_layer(synth.CONFIGS[args.config], args.seed)
+        if args.ablation:
+            # the compilations of Sec. 6.2 on the same kernel: every signed term's
+            # factor applied on its own, then grouping, then sharing whole sums,
+            # then sharing partly overlapping sums as well (the default plan)
+            # (all four on the same buffers, interleaved: see time_plan_variants)
+            variants = (("per-contribution", fiona.FIONA_PLAN_PER_CONTRIBUTION),
+                        ("+grouping", fiona.FIONA_PLAN_NO_SHARING),
+                        ("+sharing", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
+                        ("+partial sharing", 0))
+            timed = time_plan_variants(layer, dev, args.steps, args.warmup, stream, variants, padded=pad_mode)
+            abl = []
+            for name, _ in variants:
+                ms, c = timed[name]
+                abl.append({"plan": name, "ms_per_step": round(ms, 4), "value": round(layer.ct_terms / (ms * 1e-3), 1),
+                            "scalar_products": c["n_use"], "pmult": c["pmult_grouped"] - c["n_use"],
+                            "addsub": c["addsub_partial"], "common_terms": c["n_partial"]})
+            for rec in abl:
+                rec["speedup_vs_per_contribution"] = round(abl[0]["ms_per_step"] / rec["ms_per_step"], 3)
+            extra["ablation"] = {"layer": args.config, "plans": abl}
+        if args.rescale:
+            extra["rescale"] = dict(time_rescale(layer, dev, args.steps, args.warmup, stream), layer=args.config)
+        if args.rotate:
+            extra["rotate"] = dict(time_rotate(layer, dev, args.steps, args.warmup, stream), layer=args.config)
+    # each layer's raw-term multiply-adds against the register-only rate
     mb = time_mac_microbench(stream)
-    hy_words = layer.n_pm * cfg.L * cfg.N / (hy_ms * 1e-3)
-    mac_rate = {"raw_words_per_s_hybrid": round(hy_words, 1), "raw_words_per_s_register_only": mb["words_per_s"],
-                "frac": round(hy_words / mb["words_per_s"], 4), "microbench": mb}
+    for r in records:
+        w = r.pop("raw_words_per_s_hybrid")
+        r["mac_rate_frac"] = round(w / mb["words_per_s"], 4)
+    streams = None if args.no_streams else time_streams(stream)
     wall = time.perf_counter() - t_wall0
 
-    traffic = measured_traffic(cfg.name, "hybrid")
-    n_launch = len(hy_chunks)
+    hy = head["hybrid"]
     result = {
-        "metric": "ct-terms/sec and achieved HBM GB/s (hybrid vs all-PMult), N=2^16 layers, 1 GPU",
-        "value": round(hy_value, 1),
+        "metric": METRIC,
+        "value": hy["value"],
         "unit": "ct-terms/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(hy_ms, 4),
+        "ms_per_step": hy["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u64",
         "data": "synthetic (seeded counter-based generator, uniform residues; no dataset or weights)",
-        "config": {"workload": "%s: %s" % (cfg.name, cfg.description), "N": cfg.N, "L": cfg.L,
-                   "n_in": cfg.n_in, "n_out": cfg.n_out, "terms_per_output": cfg.T, "group": cfg.g,
-                   "ternary_groups": layer.n_group, "raw_terms": layer.n_pm, "ct_terms": layer.ct_terms,
-                   "chunks": n_launch, "seed": args.seed,
-                   "pt_pitch_words": hy_pitch, "pt_row_words": cfg.L * cfg.N},
-        "achieved_alg_GBps": round(hy_gbs, 1),
-        "launch_ms": {"min": round(sum(c["ms_min"] for c in hy_chunks), 4),
-                      "median": round(sum(c["ms_median"] for c in hy_chunks), 4),
-                      "max": round(sum(c["ms_max"] for c in hy_chunks), 4)},
-        "roofline": {"bound": "hbm", "achieved": round(hy_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(hy_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": None if traffic is None else round(traffic),
-                     "alg_bytes_per_launch": hy_bytes // n_launch,
-                     "kernel": " + ".join(hy_kernels)},
-        "all_pmult": allpm,
-        "hybrid_chunks": hy_chunks if n_launch > 1 else None,
-        "ablation": ablation,
-        "rescale": rescale,
-        "rotate": rotate,
-        "mac_rate": mac_rate,
+        "config": {"workload": "%s: %s" % (head["layer"], head["description"]), "N": head["N"], "L": head["L"],
+                   "n_in": head["n_in"], "n_out": head["n_out"], "terms_per_output": head["terms_per_output"],
+                   "group": head["group"], "ct_terms": head["ct_terms"], "chunks": hy["chunks"],
+                   "seed": args.seed, "rounds": args.rounds,
+                   "step": "every output chunk once: sum over chunks of the median launch time"},
+        "roofline": hy["roofline"],
+        "speedup_hybrid_vs_allpmult": head["speedup_hybrid_vs_allpmult"],
+        "layers": records,
+        "streams": streams,
+        "mac_microbench": mb,
         "gpu_wall_s": round(wall, 2),
     }
+    result.update(extra)
     if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on a sample (about 10 s)")
-        result["cpu_baseline"] = cpu_baseline(layer)
-        result["cpu_baseline"]["value"] = round(result["cpu_baseline"]["value"], 1)
+        log("[bench] timing the CPU oracle on a sample of %s (about 10 s)" % head["layer"])
+        cb = cpu_baseline(synth.make_layer(synth.CONFIGS[head["layer"]], args.seed))
+        cb["value"] = round(cb["value"], 1)
+        result["cpu_baseline"] = cb
     print(json.dumps(result), flush=True)
 
 

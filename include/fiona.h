@@ -91,6 +91,9 @@ void fiona_ctx_destroy(fiona_ctx *ctx);
 #define FIONA_PLAN_NO_OUTPUT_BURSTS 32u    /* store each output as soon as it is finished instead of
                                               buffering a round of outputs in LDS and writing them together
                                               (the default when outputs are at least 2.5% of the bytes) */
+#define FIONA_PLAN_CHECK_INPUTS 64u        /* a checking plan: it keeps the layer's signs, and every
+                                              fiona_hybrid_linear call checks its inputs' preconditions on the
+                                              host first (synchronously; see fiona_plan_check_inputs) */
 
 /*
  * One routed layer, in the raw per-(output, term) form the offline compiler
@@ -203,6 +206,29 @@ typedef struct fiona_plan_stats_t {
 int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);
 
 /*
+ * fiona_plan_check_inputs: the preconditions of fiona_hybrid_linear that a
+ * checking plan (FIONA_PLAN_CHECK_INPUTS) enforces, tested on host copies of
+ * the call's arrays (Sec. 2.2: the plan is fixed offline from the weights,
+ * so the signs a call passes must be the signs the plan was compiled from):
+ *   signs   host, [n_member] int8: must equal the layer description's mem_sign
+ *   scales  host, [n_scale] uint64: each < 2^20
+ *   in      host or NULL, [n_in][2][L][N] uint64: each < 2^50
+ *   pt      host or NULL, [n_pt] rows at the plan's pitch: each word of a
+ *           row's first L*N < 2^50
+ * Returns FIONA_OK, FIONA_ERR_PRECONDITION (the first failing check), or
+ * FIONA_ERR_ARG (a null plan or array with a nonzero size, or a plan made
+ * without FIONA_PLAN_CHECK_INPUTS, which keeps no signs).  Host only; works
+ * with a host-only plan.
+ * A checking plan's fiona_hybrid_linear copies ternary_groups, scales,
+ * in_cts and pt_diags back to the host (on its stream, then waits for it),
+ * runs this check, and returns FIONA_ERR_PRECONDITION without launching
+ * anything if it fails.  It is a debugging aid: it allocates host memory
+ * and is as slow as copying every input.
+ */
+int fiona_plan_check_inputs(const fiona_plan *plan, const int8_t *signs, const uint64_t *scales, const uint64_t *in,
+                            const uint64_t *pt);
+
+/*
  * fiona_hybrid_linear: evaluate the layer (the hot path).
  *   in_cts          device, [n_in][2][L][N] uint64, every value < 2^50
  *                   (CKKS residues are < q_l)
@@ -221,9 +247,12 @@ int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);
  * Asynchronous: returns once the kernel is queued; the buffers must stay
  * valid and unchanged until the stream reaches it.  Allocates nothing.
  * Results are exact (bit-identical to evaluating every term on its own mod q_l).
- * Input ranges above are preconditions that are not checked.  Errors
- * (nothing is launched): FIONA_ERR_ARG (null pointer with a nonzero size),
- * FIONA_ERR_ALIGN, FIONA_ERR_ALIAS, FIONA_ERR_NODEVICE, FIONA_ERR_HIP (launch).
+ * Input ranges and signs above are preconditions, checked only by a checking
+ * plan (FIONA_PLAN_CHECK_INPUTS).  Device pointers need 8-byte alignment
+ * (every access is an 8-byte word).  Errors (nothing is launched):
+ * FIONA_ERR_ARG (null pointer with a nonzero size), FIONA_ERR_ALIGN,
+ * FIONA_ERR_ALIAS, FIONA_ERR_NODEVICE, FIONA_ERR_PRECONDITION (checking plans),
+ * FIONA_ERR_HIP (launch, or a checking plan's copies).
  */
 int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
                         const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
@@ -356,6 +385,21 @@ int fiona_hoisted_rotate(const fiona_rotator *rotator, const uint64_t *ct, uint3
  */
 int fiona_mac_microbench(uint32_t blocks, uint32_t chunks, uint64_t *sink, hipStream_t stream);
 uint64_t fiona_mac_microbench_words(uint32_t blocks, uint32_t chunks);
+
+/*
+ * Measurement helpers (not part of the weighted sum): the HBM bandwidth of a
+ * plain contiguous read and of a plain copy, the ceilings the kernels' rates
+ * are set against.  Grid-stride loops over 16-byte words on blocks
+ * workgroups of 256 threads, nontemporal accesses.
+ * fiona_stream_read: reads words (even) uint64 words of src (device, 16-byte
+ *   aligned) and writes one word per workgroup to sink (device, blocks words).
+ * fiona_stream_copy: dst[i] = src[i] for words (even) words (device, 16-byte
+ *   aligned, not overlapping).
+ * Asynchronous on stream; allocate nothing.  Errors: FIONA_ERR_ARG,
+ * FIONA_ERR_ALIGN, FIONA_ERR_ALIAS (copy), FIONA_ERR_HIP.
+ */
+int fiona_stream_read(const uint64_t *src, uint64_t words, uint32_t blocks, uint64_t *sink, hipStream_t stream);
+int fiona_stream_copy(const uint64_t *src, uint64_t *dst, uint64_t words, uint32_t blocks, hipStream_t stream);
 
 /*
  * Checking helper (no device needed): replays the memory accesses of one

@@ -29,6 +29,7 @@ FIONA_PLAN_NO_LDS_SUMS = 4
 FIONA_PLAN_NO_PARTIAL_SHARING = 8
 FIONA_PLAN_PER_CONTRIBUTION = 16
 FIONA_PLAN_NO_OUTPUT_BURSTS = 32
+FIONA_PLAN_CHECK_INPUTS = 64
 
 FIONA_ERR_PRECONDITION = -9
 FIONA_ERR_BOUNDS = -10
@@ -381,3 +382,43 @@ def check_ntt_offsets(op: str, N: int, L: int, moduli, capacity: int, n_call: in
     rc = L_.fiona_check_ntt_offsets({"rescale": 0, "rotate": 1}[op], int(N), int(L), ctypes.cast(mods, ctypes.c_void_p),
                                     int(capacity), int(n_call), int(out_shrink), msg, 512)
     return rc, msg.value.decode()
+
+
+def stream_read(src_t, blocks: int, sink_t, stream=None) -> int:
+    """fiona_stream_read over all of src_t (8-byte elements, an even count);
+    returns the bytes read."""
+    L_ = lib()
+    L_.fiona_stream_read.restype = ctypes.c_int
+    L_.fiona_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p,
+                                     ctypes.c_void_p]
+    if sink_t.numel() < blocks:
+        raise ValueError("sink holds fewer than blocks words")
+    _check(L_.fiona_stream_read(_dptr(src_t, "src", 8), src_t.numel(), int(blocks), _dptr(sink_t, "sink", 8),
+                                _stream_handle(stream)), "fiona_stream_read")
+    return src_t.numel() * 8
+
+
+def stream_copy(src_t, dst_t, blocks: int, stream=None) -> int:
+    """fiona_stream_copy of all of src_t into dst_t; returns the bytes moved (read + written)."""
+    L_ = lib()
+    L_.fiona_stream_copy.restype = ctypes.c_int
+    L_.fiona_stream_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
+                                     ctypes.c_void_p]
+    if dst_t.numel() < src_t.numel():
+        raise ValueError("dst is smaller than src")
+    _check(L_.fiona_stream_copy(_dptr(src_t, "src", 8), _dptr(dst_t, "dst", 8), src_t.numel(), int(blocks),
+                                _stream_handle(stream)), "fiona_stream_copy")
+    return 2 * src_t.numel() * 8
+
+
+def plan_check_inputs(plan: Plan, signs, scales, x=None, pt=None) -> int:
+    """fiona_plan_check_inputs on host arrays (NumPy): signs int8 [n_member],
+    scales uint64 [n_scale], x uint64 [n_in][2][L][N] or None, pt uint64 rows at
+    the plan's pitch or None.  Returns the status (0, FIONA_ERR_PRECONDITION, ...)."""
+    L_ = lib()
+    L_.fiona_plan_check_inputs.restype = ctypes.c_int
+    L_.fiona_plan_check_inputs.argtypes = [ctypes.c_void_p] * 5
+    keep = [np.ascontiguousarray(signs, dtype=np.int8), np.ascontiguousarray(scales, dtype=np.uint64)]
+    keep += [None if a is None else np.ascontiguousarray(a, dtype=np.uint64) for a in (x, pt)]
+    ptrs = [None if a is None or not a.size else a.ctypes.data for a in keep]
+    return int(L_.fiona_plan_check_inputs(plan.handle, *ptrs))

@@ -81,6 +81,7 @@ struct fiona_plan {
   uint32_t n_uses = 0;
   std::vector<uint2> members;
   std::vector<uint4> blocks;   // word blocks: common partial sums, resident sums, uses (see PackParams)
+  std::vector<int8_t> signs;   // a checking plan: the layer description's mem_sign
   void *dev = nullptr;
   int device = -1;
   // device pointers into dev
@@ -726,6 +727,9 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   P->n_scale = desc->n_scale;
   P->flags = desc->flags;
   try {
+    const uint32_t n_group = desc->grp_off[desc->n_out];
+    if ((desc->flags & FIONA_PLAN_CHECK_INPUTS) && n_group)
+      P->signs.assign(desc->mem_sign, desc->mem_sign + desc->grp_mem_off[n_group]);
     rc = compile_plan(P, desc);
   } catch (...) {
     rc = FIONA_ERR_NOMEM;
@@ -781,6 +785,25 @@ int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out) {
   return FIONA_OK;
 }
 
+int fiona_plan_check_inputs(const fiona_plan *plan, const int8_t *signs, const uint64_t *scales, const uint64_t *in,
+                            const uint64_t *pt) {
+  if (!plan || !(plan->flags & FIONA_PLAN_CHECK_INPUTS)) return FIONA_ERR_ARG;
+  if ((plan->n_member_desc && !signs) || (plan->n_scale && !scales)) return FIONA_ERR_ARG;
+  if (plan->n_member_desc && std::memcmp(signs, plan->signs.data(), plan->n_member_desc) != 0)
+    return FIONA_ERR_PRECONDITION;
+  for (uint32_t c = 0; c < plan->n_scale; ++c)
+    if (scales[c] >> FIONA_SCALE_BITS) return FIONA_ERR_PRECONDITION;
+  const size_t LN = (size_t)plan->ctx->L * plan->ctx->N;
+  if (in)
+    for (size_t w = 0; w < (size_t)plan->n_in * 2 * LN; ++w)
+      if (in[w] >> FIONA_MODULUS_BITS) return FIONA_ERR_PRECONDITION;
+  if (pt)
+    for (size_t r = 0; r < plan->n_pt; ++r)
+      for (size_t w = 0; w < LN; ++w)
+        if (pt[r * plan->pt_pitch + w] >> FIONA_MODULUS_BITS) return FIONA_ERR_PRECONDITION;
+  return FIONA_OK;
+}
+
 int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
                         const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
                         hipStream_t stream) {
@@ -807,6 +830,24 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
   if (plan->n_out == 0) return FIONA_OK;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return FIONA_ERR_ARG;
+  if (plan->flags & FIONA_PLAN_CHECK_INPUTS) {   // a checking plan: the preconditions, on host copies
+    int rc = FIONA_OK;
+    try {
+      std::vector<int8_t> hs(sign_bytes);
+      std::vector<uint64_t> hc(plan->n_scale), hi(in_bytes / 8), hp(pt_bytes / 8);
+      auto back = [&](void *dst, const void *src, size_t n) {
+        return n == 0 || hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToHost, stream) == hipSuccess;
+      };
+      if (!back(hs.data(), ternary_groups, sign_bytes) || !back(hc.data(), scales, scale_bytes) ||
+          !back(hi.data(), in_cts, in_bytes) || !back(hp.data(), pt_diags, pt_bytes) ||
+          hipStreamSynchronize(stream) != hipSuccess)
+        return FIONA_ERR_HIP;
+      rc = fiona_plan_check_inputs(plan, hs.data(), hc.data(), hi.data(), pt_bytes ? hp.data() : nullptr);
+    } catch (...) {
+      return FIONA_ERR_NOMEM;
+    }
+    if (rc != FIONA_OK) return rc;
+  }
   const uint32_t n_blocks = (uint32_t)plan->blocks.size();
   if (n_blocks) {   // this call's signs and scales: the word blocks
     PackParams pp;

@@ -51,9 +51,76 @@ __global__ void __launch_bounds__(kMicroThreads) mac_microbench_kernel(uint32_t 
   sink[t] = a0.A0 ^ a0.A1 ^ a0.A2 ^ a0.A3 ^ a1.A0 ^ a1.A1 ^ a1.A2 ^ a1.A3;
 }
 
+typedef uint32_t sv4 __attribute__((ext_vector_type(4)));
+
+// Stream probes: the HBM bandwidth a plain contiguous read and a plain copy
+// reach, as ceilings to set the kernels' rates against.  Grid-stride over
+// 16-byte words, four loads in flight per thread, nontemporal loads and
+// stores (each word is touched once).  The read probe folds what it reads
+// into one word per workgroup, so that no load can be dropped.
+__global__ void __launch_bounds__(kMicroThreads) stream_read_kernel(const sv4 *__restrict__ src, uint64_t n16,
+                                                                    uint64_t *__restrict__ sink) {
+  const uint64_t step = (uint64_t)gridDim.x * kMicroThreads * 4;
+  uint32_t acc = 0;
+  for (uint64_t i = (uint64_t)blockIdx.x * kMicroThreads * 4 + threadIdx.x; i < n16; i += step) {
+    sv4 v[4];
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) {
+      const uint64_t j = i + u * kMicroThreads;
+      v[u] = j < n16 ? __builtin_nontemporal_load(src + j) : (sv4){0, 0, 0, 0};
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  __shared__ uint32_t red[kMicroThreads];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t a = 0;
+    for (uint32_t t = 0; t < kMicroThreads; ++t) a ^= red[t];
+    sink[blockIdx.x] = a;
+  }
+}
+
+__global__ void __launch_bounds__(kMicroThreads) stream_copy_kernel(const sv4 *__restrict__ src,
+                                                                    sv4 *__restrict__ dst, uint64_t n16) {
+  const uint64_t step = (uint64_t)gridDim.x * kMicroThreads * 4;
+  for (uint64_t i = (uint64_t)blockIdx.x * kMicroThreads * 4 + threadIdx.x; i < n16; i += step) {
+    sv4 v[4];
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) {
+      const uint64_t j = i + u * kMicroThreads;
+      v[u] = j < n16 ? __builtin_nontemporal_load(src + j) : (sv4){0, 0, 0, 0};
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) {
+      const uint64_t j = i + u * kMicroThreads;
+      if (j < n16) __builtin_nontemporal_store(v[u], dst + j);
+    }
+  }
+}
+
 }  // namespace fiona
 
 extern "C" {
+
+int fiona_stream_read(const uint64_t *src, uint64_t words, uint32_t blocks, uint64_t *sink, hipStream_t stream) {
+  if (!src || !sink || blocks == 0 || words == 0 || (words & 1u)) return FIONA_ERR_ARG;
+  if ((uintptr_t)src & 15u) return FIONA_ERR_ALIGN;
+  hipLaunchKernelGGL(fiona::stream_read_kernel, dim3(blocks), dim3(fiona::kMicroThreads), 0, stream,
+                     (const fiona::sv4 *)src, words / 2, sink);
+  return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
+}
+
+int fiona_stream_copy(const uint64_t *src, uint64_t *dst, uint64_t words, uint32_t blocks, hipStream_t stream) {
+  if (!src || !dst || blocks == 0 || words == 0 || (words & 1u)) return FIONA_ERR_ARG;
+  if (((uintptr_t)src | (uintptr_t)dst) & 15u) return FIONA_ERR_ALIGN;
+  const uintptr_t a = (uintptr_t)src, b = (uintptr_t)dst;
+  if (a < b + words * 8 && b < a + words * 8) return FIONA_ERR_ALIAS;
+  hipLaunchKernelGGL(fiona::stream_copy_kernel, dim3(blocks), dim3(fiona::kMicroThreads), 0, stream,
+                     (const fiona::sv4 *)src, (fiona::sv4 *)dst, words / 2);
+  return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
+}
 
 uint64_t fiona_mac_microbench_words(uint32_t blocks, uint32_t chunks) {
   return (uint64_t)blocks * fiona::kMicroThreads * chunks * fiona::kChunkTerms;
