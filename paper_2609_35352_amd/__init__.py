@@ -31,6 +31,7 @@ FIONA_PLAN_PER_CONTRIBUTION = 16
 FIONA_PLAN_NO_OUTPUT_BURSTS = 32
 FIONA_PLAN_CHECK_INPUTS = 64
 
+FIONA_ERR_ARG = -1
 FIONA_ERR_PRECONDITION = -9
 FIONA_ERR_BOUNDS = -10
 

@@ -701,6 +701,75 @@ int upload_plan(fiona_plan *P) {
   return FIONA_OK;
 }
 
+// Byte sizes of one call's arrays.
+struct CallBytes {
+  size_t in, pt, out, sign, scale;
+};
+
+// The argument checks of a call (nothing is launched on an error).
+int check_call(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags, const int8_t *ternary_groups,
+               const uint64_t *scales, const uint64_t *out_cts, CallBytes &b) {
+  if (!plan) return FIONA_ERR_ARG;
+  if (!plan->dev) return FIONA_ERR_NODEVICE;
+  const fiona_ctx *C = plan->ctx;
+  const size_t LN = (size_t)C->L * C->N;
+  b.in = (size_t)plan->n_in * 2 * LN * 8;
+  b.pt = plan->n_pt ? ((size_t)(plan->n_pt - 1) * plan->pt_pitch + LN) * 8 : 0;
+  b.out = (size_t)plan->n_out * 2 * LN * 8;
+  b.sign = plan->n_member_desc;
+  b.scale = (size_t)plan->n_scale * 8;
+  if (!in_cts) return FIONA_ERR_ARG;
+  if (plan->n_out && !out_cts) return FIONA_ERR_ARG;
+  if (!plan->pm.empty() && !pt_diags) return FIONA_ERR_ARG;
+  if (plan->any_signed && (!ternary_groups || !scales)) return FIONA_ERR_ARG;
+  if (((uintptr_t)in_cts | (uintptr_t)pt_diags | (uintptr_t)scales | (uintptr_t)out_cts) & 7u)
+    return FIONA_ERR_ALIGN;
+  if (ranges_overlap(out_cts, b.out, in_cts, b.in) || ranges_overlap(out_cts, b.out, pt_diags, b.pt) ||
+      ranges_overlap(out_cts, b.out, ternary_groups, b.sign) || ranges_overlap(out_cts, b.out, scales, b.scale))
+    return FIONA_ERR_ALIAS;
+  if (plan->n_out == 0) return FIONA_OK;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return FIONA_ERR_ARG;
+  return FIONA_OK;
+}
+
+// The launches of one call: the sign-packing kernel writes this call's word
+// blocks at words (plan->blocks.size() blocks of kSumWords words), then the
+// main kernel reads them.
+int enqueue_layer(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
+                  const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts, uint32_t *words,
+                  const CallBytes &b, hipStream_t stream) {
+  const uint32_t n_blocks = (uint32_t)plan->blocks.size();
+  if (n_blocks) {   // this call's signs and scales: the word blocks
+    PackParams pp;
+    pp.signs = ternary_groups;
+    pp.members = plan->d_members;
+    pp.blocks = plan->d_blocks;
+    pp.words = words;
+    pp.scales = scales;
+    pp.n_blocks = n_blocks;
+    pp.zero_row = plan->shape.zero_row;
+    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((n_blocks + 3) / 4), dim3(256), 0, stream, pp);
+    if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
+  }
+  auto kernel = plan->nw == 16 ? fiona::hybrid_linear_kernel<16> : fiona::hybrid_linear_kernel<8>;
+  fiona::KPlan kp;
+  kp.limbs = plan->d_limbs;
+  kp.items = plan->d_items;
+  kp.dest = plan->d_dest;
+  kp.waves = plan->d_waves;
+  kp.rounds = plan->d_rounds;
+  kp.flush = plan->d_flush;
+  kp.splits = plan->d_splits;
+  kp.pm = plan->d_pm;
+  kp.words = words;
+  hipLaunchKernelGGL(kernel, dim3(plan->grid), dim3(plan->nw * 64), plan->lds_bytes, stream, in_cts, pt_diags,
+                     out_cts, kp, plan->shape, (const void *)((const char *)pt_diags + b.pt),
+                     (const void *)((const char *)out_cts + b.out));
+  if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
+  return FIONA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -807,76 +876,27 @@ int fiona_plan_check_inputs(const fiona_plan *plan, const int8_t *signs, const u
 int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
                         const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
                         hipStream_t stream) {
-  if (!plan) return FIONA_ERR_ARG;
-  if (!plan->dev) return FIONA_ERR_NODEVICE;
-  const fiona_ctx *C = plan->ctx;
-  const size_t LN = (size_t)C->L * C->N;
-  const size_t in_bytes = (size_t)plan->n_in * 2 * LN * 8;
-  const size_t pt_bytes = plan->n_pt ? ((size_t)(plan->n_pt - 1) * plan->pt_pitch + LN) * 8 : 0;
-  const size_t out_bytes = (size_t)plan->n_out * 2 * LN * 8;
-  const size_t sign_bytes = plan->n_member_desc;
-  const size_t scale_bytes = (size_t)plan->n_scale * 8;
-  if (!in_cts) return FIONA_ERR_ARG;
-  if (plan->n_out && !out_cts) return FIONA_ERR_ARG;
-  if (!plan->pm.empty() && !pt_diags) return FIONA_ERR_ARG;
-  if (plan->any_signed && (!ternary_groups || !scales)) return FIONA_ERR_ARG;
-  if (((uintptr_t)in_cts | (uintptr_t)pt_diags | (uintptr_t)scales | (uintptr_t)out_cts) & 7u)
-    return FIONA_ERR_ALIGN;
-  if (ranges_overlap(out_cts, out_bytes, in_cts, in_bytes) ||
-      ranges_overlap(out_cts, out_bytes, pt_diags, pt_bytes) ||
-      ranges_overlap(out_cts, out_bytes, ternary_groups, sign_bytes) ||
-      ranges_overlap(out_cts, out_bytes, scales, scale_bytes))
-    return FIONA_ERR_ALIAS;
-  if (plan->n_out == 0) return FIONA_OK;
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return FIONA_ERR_ARG;
+  CallBytes b;
+  int rc = check_call(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, b);
+  if (rc != FIONA_OK || plan->n_out == 0) return rc;
   if (plan->flags & FIONA_PLAN_CHECK_INPUTS) {   // a checking plan: the preconditions, on host copies
-    int rc = FIONA_OK;
     try {
-      std::vector<int8_t> hs(sign_bytes);
-      std::vector<uint64_t> hc(plan->n_scale), hi(in_bytes / 8), hp(pt_bytes / 8);
+      std::vector<int8_t> hs(b.sign);
+      std::vector<uint64_t> hc(plan->n_scale), hi(b.in / 8), hp(b.pt / 8);
       auto back = [&](void *dst, const void *src, size_t n) {
         return n == 0 || hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToHost, stream) == hipSuccess;
       };
-      if (!back(hs.data(), ternary_groups, sign_bytes) || !back(hc.data(), scales, scale_bytes) ||
-          !back(hi.data(), in_cts, in_bytes) || !back(hp.data(), pt_diags, pt_bytes) ||
+      if (!back(hs.data(), ternary_groups, b.sign) || !back(hc.data(), scales, b.scale) ||
+          !back(hi.data(), in_cts, b.in) || !back(hp.data(), pt_diags, b.pt) ||
           hipStreamSynchronize(stream) != hipSuccess)
         return FIONA_ERR_HIP;
-      rc = fiona_plan_check_inputs(plan, hs.data(), hc.data(), hi.data(), pt_bytes ? hp.data() : nullptr);
+      rc = fiona_plan_check_inputs(plan, hs.data(), hc.data(), hi.data(), b.pt ? hp.data() : nullptr);
     } catch (...) {
       return FIONA_ERR_NOMEM;
     }
     if (rc != FIONA_OK) return rc;
   }
-  const uint32_t n_blocks = (uint32_t)plan->blocks.size();
-  if (n_blocks) {   // this call's signs and scales: the word blocks
-    PackParams pp;
-    pp.signs = ternary_groups;
-    pp.members = plan->d_members;
-    pp.blocks = plan->d_blocks;
-    pp.words = plan->d_words;
-    pp.scales = scales;
-    pp.n_blocks = n_blocks;
-    pp.zero_row = plan->shape.zero_row;
-    hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((n_blocks + 3) / 4), dim3(256), 0, stream, pp);
-    if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
-  }
-  auto kernel = plan->nw == 16 ? fiona::hybrid_linear_kernel<16> : fiona::hybrid_linear_kernel<8>;
-  fiona::KPlan kp;
-  kp.limbs = plan->d_limbs;
-  kp.items = plan->d_items;
-  kp.dest = plan->d_dest;
-  kp.waves = plan->d_waves;
-  kp.rounds = plan->d_rounds;
-  kp.flush = plan->d_flush;
-  kp.splits = plan->d_splits;
-  kp.pm = plan->d_pm;
-  kp.words = plan->d_words;
-  hipLaunchKernelGGL(kernel, dim3(plan->grid), dim3(plan->nw * 64), plan->lds_bytes, stream, in_cts, pt_diags,
-                     out_cts, kp, plan->shape, (const void *)((const char *)pt_diags + pt_bytes),
-                     (const void *)((const char *)out_cts + out_bytes));
-  if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
-  return FIONA_OK;
+  return enqueue_layer(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, plan->d_words, b, stream);
 }
 
 }  // extern "C"

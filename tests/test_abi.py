@@ -343,3 +343,35 @@ def test_partial_sharing_with_repeated_inputs():
     assert st["n_member_nonzero"] == 4 * n_out
     assert st["addsub_shared"] == 3 * n_out
     assert st["n_partial"] == 0 and st["addsub_partial"] == 3 * n_out
+
+
+def test_checking_plan_preconditions_on_the_host():
+    """A checking plan keeps the layer's signs: the signs a call passes must be
+    the ones the plan was compiled from (Sec. 2.2, a plan fixed offline), scales
+    below 2^20, inputs and plaintext words below 2^50."""
+    layer = synth.make_layer(synth.LayerConfig("chk", N=64, L=2, n_in=6, n_out=3, T=12, g=3, ternary=0.5),
+                             3, moduli=synth.ntt_primes(64, 2))
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    plan = fiona.Plan.from_layer(ctx, layer, flags=HOST | fiona.FIONA_PLAN_CHECK_INPUTS)
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    ok = fiona.plan_check_inputs
+    assert ok(plan, layer.mem_sign, layer.scales, x, pt) == 0
+    assert ok(plan, layer.mem_sign, layer.scales) == 0                     # signs and scales only
+    nz = int(np.nonzero(layer.mem_sign)[0][0])
+    for change in (lambda s: s.__setitem__(nz, -s[nz]), lambda s: s.__setitem__(nz, 0),
+                   lambda s: s.__setitem__(int(np.nonzero(layer.mem_sign == 0)[0][0]), 1)):
+        s2 = layer.mem_sign.copy()
+        change(s2)
+        assert ok(plan, s2, layer.scales, x, pt) == fiona.FIONA_ERR_PRECONDITION
+    sc = layer.scales.copy()
+    sc[-1] = 1 << 20
+    assert ok(plan, layer.mem_sign, sc) == fiona.FIONA_ERR_PRECONDITION
+    x2 = x.copy()
+    x2[1, 1, 1, 5] = np.uint64(1 << 50)
+    assert ok(plan, layer.mem_sign, layer.scales, x2, pt) == fiona.FIONA_ERR_PRECONDITION
+    pt2 = pt.copy()
+    pt2[-1, -1, -1] = np.uint64(2 ** 64 - 1)
+    assert ok(plan, layer.mem_sign, layer.scales, x, pt2) == fiona.FIONA_ERR_PRECONDITION
+    # a plan made without the flag keeps no signs
+    plain = fiona.Plan.from_layer(ctx, layer, flags=HOST)
+    assert ok(plain, layer.mem_sign, layer.scales) == fiona.FIONA_ERR_ARG

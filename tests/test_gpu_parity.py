@@ -541,3 +541,31 @@ def test_full_size_large_contiguous_tiles(dev, chunk):
                              % (chunk, len(bad), a + j, p, limbs[i], coeffs[i]))
     del out_t, in_t
     torch.cuda.empty_cache()
+
+
+def test_checking_plan(dev):
+    """A checking plan (FIONA_PLAN_CHECK_INPUTS) computes the same outputs; a
+    call whose signs differ from the plan's, or whose input breaks the 2^50
+    bound, is refused before anything is launched (the output keeps its fill)."""
+    import torch
+    layer = _small_layer("ragged_pool")
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    out_t, in_t, pt_t, plan = _run(layer, dev, x, pt, flags=fiona.FIONA_PLAN_CHECK_INPUTS)
+    _assert_equal(_host(out_t, layer), expect, "checking plan")
+    signs2 = layer.mem_sign.copy()
+    nz = int(np.nonzero(signs2)[0][0])
+    signs2[nz] = -signs2[nz]
+    scale_t = _to_dev(layer.scales, np.int64, dev)
+    out2 = torch.full_like(out_t, -1)
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.hybrid_linear(plan, in_t, pt_t, _to_dev(signs2, np.int8, dev), scale_t, out2)
+    assert e.value.status == fiona.FIONA_ERR_PRECONDITION
+    x2 = x.copy()
+    x2[-1, 1, -1, -1] = np.uint64(1 << 50)
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.hybrid_linear(plan, _to_dev(x2, np.int64, dev), pt_t, _to_dev(layer.mem_sign, np.int8, dev), scale_t,
+                            out2)
+    assert e.value.status == fiona.FIONA_ERR_PRECONDITION
+    torch.cuda.synchronize()
+    assert bool((out2 == -1).all())
