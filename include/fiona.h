@@ -259,6 +259,28 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
                         hipStream_t stream);
 
 /*
+ * fiona_hybrid_linear_static: fiona_hybrid_linear for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, results and errors.
+ * The per-call word blocks (the signed sums' member rows and the uses'
+ * scales, written by the sign-packing kernel on every call) go to a
+ * library-owned static device array of 4 MiB per device instead of the
+ * plan's workspace; the array's address is looked up on the first call on a
+ * device and kept until the process ends.  Allocates nothing (neither device
+ * nor host memory).  Every call on one device shares its array and leaves its
+ * blocks there; each call writes every block it reads before reading it, so
+ * nothing needs clearing, but calls that overlap on one device (two streams,
+ * or two host threads) race and must be serialized by the caller.
+ * Errors, besides fiona_hybrid_linear's: FIONA_ERR_UNSUPPORTED if the plan's
+ * word blocks exceed 4 MiB (more than 16384 common terms, resident sums and
+ * uses); FIONA_ERR_ARG for a checking plan (FIONA_PLAN_CHECK_INPUTS), whose
+ * check copies into host memory.
+ */
+int fiona_hybrid_linear_static(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
+                               const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
+                               hipStream_t stream);
+
+/*
  * Rescale epilogue: divide ciphertexts by the last modulus q_t = q_{L-1} of the
  * chain, with rounding, and drop that limb (CKKS rescaling, paper Sec. 2
  * "Levels and Bootstrapping").  Sec. 4.2 "Combining the Signed and Raw

@@ -202,10 +202,8 @@ def _dptr(t, name, elem_size):
     return t.data_ptr()
 
 
-def hybrid_linear(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t, stream=None) -> None:
-    """fiona_hybrid_linear on torch device tensors (queued on ``stream``, default: current)."""
-    import torch
-
+def _call_ptrs(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t):
+    """The device pointers of one call, after checking the tensors' sizes."""
     N, L = plan.ctx.N, plan.ctx.L
     sizes = [(in_t, "in_cts", plan.n_in * 2 * L * N), (pt_t, "pt_diags", plan.pt_words()),
              (out_t, "out_cts", plan.n_out * 2 * L * N), (sign_t, "ternary_groups", plan.n_member),
@@ -213,12 +211,14 @@ def hybrid_linear(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t, stream=None) -
     for t, name, n in sizes:
         if t is not None and t.numel() < n:
             raise ValueError("%s has %d elements, needs %d" % (name, t.numel(), n))
-    if stream is None:
-        stream = torch.cuda.current_stream()
-    s = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
-    _check(lib().fiona_hybrid_linear(plan.handle, _dptr(in_t, "in_cts", 8), _dptr(pt_t, "pt_diags", 8),
-                                     _dptr(sign_t, "ternary_groups", 1), _dptr(scale_t, "scales", 8),
-                                     _dptr(out_t, "out_cts", 8), s), "fiona_hybrid_linear")
+    return (_dptr(in_t, "in_cts", 8), _dptr(pt_t, "pt_diags", 8), _dptr(sign_t, "ternary_groups", 1),
+            _dptr(scale_t, "scales", 8), _dptr(out_t, "out_cts", 8))
+
+
+def hybrid_linear(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t, stream=None) -> None:
+    """fiona_hybrid_linear on torch device tensors (queued on ``stream``, default: current)."""
+    _check(lib().fiona_hybrid_linear(plan.handle, *_call_ptrs(plan, in_t, pt_t, sign_t, scale_t, out_t),
+                                     _stream_handle(stream)), "fiona_hybrid_linear")
 
 
 class Rescaler:
@@ -423,3 +423,13 @@ def plan_check_inputs(plan: Plan, signs, scales, x=None, pt=None) -> int:
     keep += [None if a is None else np.ascontiguousarray(a, dtype=np.uint64) for a in (x, pt)]
     ptrs = [None if a is None or not a.size else a.ctypes.data for a in keep]
     return int(L_.fiona_plan_check_inputs(plan.handle, *ptrs))
+
+
+def hybrid_linear_static(plan: Plan, in_t, pt_t, sign_t, scale_t, out_t, stream=None) -> None:
+    """fiona_hybrid_linear_static: hybrid_linear with its word blocks in the
+    library's static per-device array (allocates nothing)."""
+    L_ = lib()
+    L_.fiona_hybrid_linear_static.restype = ctypes.c_int
+    L_.fiona_hybrid_linear_static.argtypes = [ctypes.c_void_p] * 7
+    _check(L_.fiona_hybrid_linear_static(plan.handle, *_call_ptrs(plan, in_t, pt_t, sign_t, scale_t, out_t),
+                                         _stream_handle(stream)), "fiona_hybrid_linear_static")

@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <unordered_map>
 #include <vector>
@@ -701,6 +702,33 @@ int upload_plan(fiona_plan *P) {
   return FIONA_OK;
 }
 
+// The word blocks of fiona_hybrid_linear_static live in a file-scope device
+// array, one copy per device, looked up once per device (hipGetSymbolAddress
+// with that device current) and kept for the life of the process.
+constexpr size_t kScratchBytes = (size_t)4 << 20;   // 16384 word blocks
+constexpr int kScratchDevices = 64;
+std::mutex scratch_mutex;
+uint32_t *scratch_addr[kScratchDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) uint32_t scratch[kScratchBytes / sizeof(uint32_t)];
+
+namespace {
+
+// This device's copy of scratch (dev is current).
+int scratch_on(int dev, uint32_t **out) {
+  if (dev < 0 || dev >= kScratchDevices) return FIONA_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_addr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FIONA_ERR_HIP;
+    scratch_addr[dev] = (uint32_t *)p;
+  }
+  *out = scratch_addr[dev];
+  return FIONA_OK;
+}
+
 // Byte sizes of one call's arrays.
 struct CallBytes {
   size_t in, pt, out, sign, scale;
@@ -897,6 +925,22 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
     if (rc != FIONA_OK) return rc;
   }
   return enqueue_layer(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, plan->d_words, b, stream);
+}
+
+int fiona_hybrid_linear_static(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
+                               const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts,
+                               hipStream_t stream) {
+  CallBytes b;
+  int rc = check_call(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, b);
+  if (rc != FIONA_OK || plan->n_out == 0) return rc;
+  if (plan->flags & FIONA_PLAN_CHECK_INPUTS) return FIONA_ERR_ARG;   // its check copies into host memory
+  if (plan->blocks.size() * fiona::kSumWords * sizeof(uint32_t) > kScratchBytes) return FIONA_ERR_UNSUPPORTED;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return FIONA_ERR_HIP;
+  uint32_t *words = nullptr;
+  rc = scratch_on(dev, &words);
+  if (rc != FIONA_OK) return rc;
+  return enqueue_layer(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, words, b, stream);
 }
 
 }  // extern "C"

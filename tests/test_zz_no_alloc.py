@@ -1,0 +1,91 @@
+"""fiona_hybrid_linear_static (word blocks in the library's static device
+array, no allocation) against fiona_hybrid_linear, through the C ABI: two
+calls in a row, the second on a smaller layer with fewer word blocks, each
+bit-identical to the existing entry point's result (and to the oracle); the
+size limit and the checking-plan refusal."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+import paper_2609_35352_amd as fiona
+
+pytestmark = pytest.mark.gpu
+
+FIRST = synth.LayerConfig("static_first", N=512, L=3, n_in=20, n_out=40, T=80, g=8, ternary=0.7, pool=4)
+SECOND = synth.LayerConfig("static_second", N=200, L=2, n_in=10, n_out=9, T=40, g=5, ternary=0.6)
+
+
+def _dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fiona.lib()
+    return torch.device("cuda:0")
+
+
+def _t(a, dt, dev):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).view(dt)).to(dev)
+
+
+def _both(layer, dev):
+    """Outputs of the existing entry point and of the static one on the same inputs."""
+    import torch
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    plan = fiona.Plan.from_layer(ctx, layer)
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    in_t, pt_t = _t(x, np.int64, dev), _t(pt, np.int64, dev)
+    sign_t, scale_t = _t(layer.mem_sign, np.int8, dev), _t(layer.scales, np.int64, dev)
+    n = layer.n_out * 2 * layer.L * layer.N
+    ref = torch.full((n,), -1, dtype=torch.int64, device=dev)
+    got = torch.full((n,), -2, dtype=torch.int64, device=dev)
+    print("[no-alloc] %s: N=%d L=%d outputs=%d stats=%s" % (layer.cfg.name, layer.N, layer.L, layer.n_out,
+                                                            plan.stats()), flush=True)
+    fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, ref)
+    fiona.hybrid_linear_static(plan, in_t, pt_t, sign_t, scale_t, got)
+    torch.cuda.synchronize()
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    r = ref.cpu().numpy().view(np.uint64).reshape(expect.shape)
+    g = got.cpu().numpy().view(np.uint64).reshape(expect.shape)
+    return r, g, expect, plan
+
+
+def test_static_entry_point_two_calls():
+    dev = _dev()
+    a = synth.make_layer(FIRST, 3, moduli=synth.ntt_primes(512, 3))
+    b = synth.make_layer(SECOND, 4, moduli=synth.ntt_primes(256, 2))
+    ra, ga, ea, pa = _both(a, dev)
+    rb, gb, eb, pb = _both(b, dev)
+    # the second call reads fewer word blocks than the first left in the array
+    assert pb.stats()["n_use"] < pa.stats()["n_use"]
+    for name, r, g, e in (("first", ra, ga, ea), ("second", rb, gb, eb)):
+        assert np.array_equal(r, e), name + ": fiona_hybrid_linear differs from the oracle"
+        bad = np.argwhere(g != r)
+        assert not bad.size, "%s call: %d words differ, first at %s" % (name, len(bad), tuple(bad[0]))
+
+
+def test_static_entry_point_limits():
+    import torch
+    dev = _dev()
+    # 20000 uses: more word blocks than the 4 MiB array holds
+    big = synth.make_layer(synth.LayerConfig("static_big", N=64, L=1, n_in=8, n_out=20, T=8000, g=8, ternary=1.0),
+                           5, moduli=synth.ntt_primes(64, 1))
+    ctx = fiona.Ctx(big.N, big.L, big.moduli)
+    plan = fiona.Plan.from_layer(ctx, big)
+    assert plan.stats()["n_use"] > 16384
+    in_t = torch.zeros(big.n_in * 2 * big.N, dtype=torch.int64, device=dev)
+    out_t = torch.zeros(big.n_out * 2 * big.N, dtype=torch.int64, device=dev)
+    sign_t, scale_t = _t(big.mem_sign, np.int8, dev), _t(big.scales, np.int64, dev)
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.hybrid_linear_static(plan, in_t, None, sign_t, scale_t, out_t)
+    assert e.value.status == -3
+    small = synth.make_layer(SECOND, 4, moduli=synth.ntt_primes(256, 2))
+    ctx2 = fiona.Ctx(small.N, small.L, small.moduli)
+    chk = fiona.Plan.from_layer(ctx2, small, flags=fiona.FIONA_PLAN_CHECK_INPUTS)
+    x, pt = synth.input_values(small), synth.pt_values(small)
+    out2 = torch.zeros(small.n_out * 2 * small.L * small.N, dtype=torch.int64, device=dev)
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.hybrid_linear_static(chk, _t(x, np.int64, dev), _t(pt, np.int64, dev),
+                                   _t(small.mem_sign, np.int8, dev), _t(small.scales, np.int64, dev), out2)
+    assert e.value.status == fiona.FIONA_ERR_ARG
