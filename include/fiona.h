@@ -60,8 +60,10 @@ typedef enum fiona_status {
 #define FIONA_MODULUS_BITS 50      /* every modulus satisfies 2^20 < q < 2^50 */
 #define FIONA_SCALE_BITS 20        /* every integer scale c satisfies c < 2^20 */
 #define FIONA_MAX_MEMBERS 48u      /* longer ternary groups are split into exact sub-sums */
-#define FIONA_MAX_INPUTS 159u      /* input ciphertexts per layer: a 64-coefficient tile of every
-                                      input (16 B each) plus one zero row fill the 160 KiB LDS */
+#define FIONA_MAX_INPUTS 159u      /* input ciphertexts of one pass: a 64-coefficient tile of every
+                                      input (16 B each) plus one zero row fill the 160 KiB LDS; a layer
+                                      with more inputs runs in passes over input ranges */
+#define FIONA_MAX_LAYER_INPUTS 65536u   /* input ciphertexts per layer */
 
 typedef struct fiona_ctx fiona_ctx;
 typedef struct fiona_plan fiona_plan;
@@ -165,9 +167,16 @@ uint64_t fiona_pt_pitch_hint(const fiona_ctx *ctx);
  *     every sum that contains it as a single member;
  *   - uploads the compiled metadata to the current HIP device (synchronous)
  *     unless FIONA_PLAN_HOST_ONLY.
+ *   - a layer with more than FIONA_MAX_INPUTS inputs is compiled as passes
+ *     over consecutive input ranges of at most 128 inputs each: a pass takes
+ *     the raw terms and the group members whose input falls in its range (a
+ *     group spanning several ranges becomes one sub-sum per range with the
+ *     group's scale, exact since c*(U1 + U2) = c*U1 + c*U2); the first pass
+ *     stores the outputs and each later pass adds its sums to them mod q_l,
+ *     so the outputs are read and written once more per extra pass;
  * The plan keeps a reference to ctx (which must outlive it).  Errors:
  * FIONA_ERR_ARG (also a pt_pitch below L*N), FIONA_ERR_PLAN, FIONA_ERR_UNSUPPORTED
- * (more than FIONA_MAX_INPUTS inputs, or a plaintext table beyond 2^48 bytes), FIONA_ERR_NOMEM, FIONA_ERR_HIP.
+ * (more than FIONA_MAX_LAYER_INPUTS inputs, or a plaintext table beyond 2^48 bytes), FIONA_ERR_NOMEM, FIONA_ERR_HIP.
  * The plan owns a small device
  * workspace (the members of its signed sums, reordered by sign on every call),
  * so one plan must not be used by two streams at the same time.
@@ -201,6 +210,10 @@ typedef struct fiona_plan_stats_t {
   uint32_t partial_levels;         /* longest chain of common terms built from common terms */
   uint32_t output_rounds;          /* rounds of outputs per tile, each ending in one burst of stores */
   uint32_t output_buffer_rows;     /* LDS rows (outputs) buffered per round; 0 = stored directly */
+  uint32_t input_passes;           /* launches (input ranges) per call: 1 up to FIONA_MAX_INPUTS inputs;
+                                      with several, the counts above add up over the passes (a group
+                                      split over passes counts one use per pass) and the launch shape is
+                                      the widest pass's */
 } fiona_plan_stats_t;
 
 int fiona_plan_stats(const fiona_plan *plan, fiona_plan_stats_t *out);

@@ -61,7 +61,7 @@ class _Stats(ctypes.Structure):
         "pmult_per_contribution", "pmult_grouped", "addsub_unshared", "addsub_shared", "addsub_partial")] + \
         [(n, ctypes.c_uint32) for n in ("tile", "waves", "lds_bytes", "grid", "split_outputs", "segment_slots",
                                         "n_partial", "partial_levels", "output_rounds",
-                                        "output_buffer_rows")]
+                                        "output_buffer_rows", "input_passes")]
 
 
 _lib = None

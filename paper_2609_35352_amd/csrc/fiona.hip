@@ -83,6 +83,14 @@ struct fiona_plan {
   std::vector<uint2> members;
   std::vector<uint4> blocks;   // word blocks: common partial sums, resident sums, uses (see PackParams)
   std::vector<int8_t> signs;   // a checking plan: the layer description's mem_sign
+  bool any_raw = false;
+  // A layer with more inputs than the LDS of one tile holds runs in passes
+  // over ranges of its inputs: the plan then keeps one plan per pass (the
+  // first stores the outputs, the later ones add to them) and no image of
+  // its own.  A pass reads inputs in_base .. in_base + n_in - 1.
+  std::vector<fiona_plan *> passes;
+  uint32_t in_base = 0;
+  bool accumulate = false;   // a pass after the first: adds to the outputs
   void *dev = nullptr;
   int device = -1;
   // device pointers into dev
@@ -643,6 +651,7 @@ int compile_plan(fiona_plan *P, const fiona_layer_desc *d) {
   st.addsub_unshared = addsub_unshared;
   st.addsub_shared = addsub_shared;
   P->any_signed = P->n_uses > 0;
+  P->any_raw = n_pm > 0;
   return FIONA_OK;
 }
 
@@ -682,11 +691,13 @@ int upload_plan(fiona_plan *P) {
   if (hipMemcpy(P->dev, host.data(), total, hipMemcpyHostToDevice) != hipSuccess) return FIONA_ERR_HIP;
   // the kernels' LDS limit, set on the current device with every plan (cheap,
   // and correct whatever device the plan lives on)
-  if (hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<8>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          (int)kLdsBytes) != hipSuccess ||
-      hipFuncSetAttribute((const void *)fiona::hybrid_linear_kernel<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          (int)kLdsBytes) != hipSuccess)
-    return FIONA_ERR_HIP;
+  const void *kernels[4] = {(const void *)fiona::hybrid_linear_kernel<8, false>,
+                            (const void *)fiona::hybrid_linear_kernel<16, false>,
+                            (const void *)fiona::hybrid_linear_kernel<8, true>,
+                            (const void *)fiona::hybrid_linear_kernel<16, true>};
+  for (const void *k : kernels)
+    if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes) != hipSuccess)
+      return FIONA_ERR_HIP;
   unsigned char *base = (unsigned char *)P->dev;
   P->d_limbs = (const LimbConst *)(base + o_limbs);
   P->d_items = (const uint4 *)(base + o_items);
@@ -738,7 +749,7 @@ struct CallBytes {
 int check_call(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags, const int8_t *ternary_groups,
                const uint64_t *scales, const uint64_t *out_cts, CallBytes &b) {
   if (!plan) return FIONA_ERR_ARG;
-  if (!plan->dev) return FIONA_ERR_NODEVICE;
+  if (!(plan->passes.empty() ? plan->dev : plan->passes[0]->dev)) return FIONA_ERR_NODEVICE;
   const fiona_ctx *C = plan->ctx;
   const size_t LN = (size_t)C->L * C->N;
   b.in = (size_t)plan->n_in * 2 * LN * 8;
@@ -748,7 +759,7 @@ int check_call(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *p
   b.scale = (size_t)plan->n_scale * 8;
   if (!in_cts) return FIONA_ERR_ARG;
   if (plan->n_out && !out_cts) return FIONA_ERR_ARG;
-  if (!plan->pm.empty() && !pt_diags) return FIONA_ERR_ARG;
+  if (plan->any_raw && !pt_diags) return FIONA_ERR_ARG;
   if (plan->any_signed && (!ternary_groups || !scales)) return FIONA_ERR_ARG;
   if (((uintptr_t)in_cts | (uintptr_t)pt_diags | (uintptr_t)scales | (uintptr_t)out_cts) & 7u)
     return FIONA_ERR_ALIGN;
@@ -764,7 +775,7 @@ int check_call(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *p
 // The launches of one call: the sign-packing kernel writes this call's word
 // blocks at words (plan->blocks.size() blocks of kSumWords words), then the
 // main kernel reads them.
-int enqueue_layer(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
+int enqueue_one(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
                   const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts, uint32_t *words,
                   const CallBytes &b, hipStream_t stream) {
   const uint32_t n_blocks = (uint32_t)plan->blocks.size();
@@ -780,7 +791,10 @@ int enqueue_layer(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t
     hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((n_blocks + 3) / 4), dim3(256), 0, stream, pp);
     if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   }
-  auto kernel = plan->nw == 16 ? fiona::hybrid_linear_kernel<16> : fiona::hybrid_linear_kernel<8>;
+  auto kernel = plan->nw == 16 ? (plan->accumulate ? fiona::hybrid_linear_kernel<16, true>
+                                                  : fiona::hybrid_linear_kernel<16, false>)
+                                : (plan->accumulate ? fiona::hybrid_linear_kernel<8, true>
+                                                    : fiona::hybrid_linear_kernel<8, false>);
   fiona::KPlan kp;
   kp.limbs = plan->d_limbs;
   kp.items = plan->d_items;
@@ -798,36 +812,50 @@ int enqueue_layer(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t
   return FIONA_OK;
 }
 
-}  // namespace
+// A call of a plan with or without passes; words: the word blocks of each
+// pass (null: each pass's own workspace).  The passes run in turn on the
+// stream, so that a later pass adds to the outputs of the earlier ones and
+// may reuse the same word blocks.
+int enqueue_layer(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
+                  const int8_t *ternary_groups, const uint64_t *scales, uint64_t *out_cts, uint32_t *words,
+                  const CallBytes &b, hipStream_t stream) {
+  if (plan->passes.empty())
+    return enqueue_one(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, words ? words : plan->d_words, b,
+                       stream);
+  const size_t LN = (size_t)plan->ctx->L * plan->ctx->N;
+  for (const fiona_plan *S : plan->passes) {
+    CallBytes bs = b;
+    bs.in = (size_t)S->n_in * 2 * LN * 8;
+    const int rc = enqueue_one(S, in_cts + (size_t)S->in_base * 2 * LN, pt_diags, ternary_groups, scales, out_cts,
+                               words ? words : S->d_words, bs, stream);
+    if (rc != FIONA_OK) return rc;
+  }
+  return FIONA_OK;
+}
 
-extern "C" {
+// Inputs per pass of a layer with more than FIONA_MAX_INPUTS inputs: room
+// for common partial sums, resident sums and output rows beside them.
+constexpr uint32_t kPassInputs = 128;
 
-int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_plan **out) {
-  if (!out) return FIONA_ERR_ARG;
-  *out = nullptr;
-  if (!ctx || !desc) return FIONA_ERR_ARG;
-  int rc = validate_desc(desc);
-  if (rc != FIONA_OK) return rc;
-  if (desc->n_in > FIONA_MAX_INPUTS) return FIONA_ERR_UNSUPPORTED;
-  const uint64_t ln = (uint64_t)ctx->L * ctx->N;
-  const uint64_t pitch = desc->pt_pitch ? desc->pt_pitch : ln;
-  if (pitch < ln || pitch > (1ull << 45)) return FIONA_ERR_ARG;
-  // raw-term records hold 48-bit byte offsets into the plaintext table
-  if (((uint64_t)desc->n_pt * pitch) * 8 > (1ull << 48)) return FIONA_ERR_UNSUPPORTED;
+// Compiles one plan over all of d's inputs and, unless host-only, uploads it.
+// slot_map (or null): for each member of d, its index in the caller's
+// ternary_groups; n_member: the caller's member count.
+int build_plan(const fiona_ctx *ctx, const fiona_layer_desc *d, uint64_t pitch, const std::vector<uint32_t> *slot_map,
+               uint32_t n_member, fiona_plan **out) {
   fiona_plan *P = new (std::nothrow) fiona_plan;
   if (!P) return FIONA_ERR_NOMEM;
   P->ctx = ctx;
-  P->n_in = desc->n_in;
-  P->n_out = desc->n_out;
-  P->n_pt = desc->n_pt;
+  P->n_in = d->n_in;
+  P->n_out = d->n_out;
+  P->n_pt = d->n_pt;
   P->pt_pitch = pitch;
-  P->n_scale = desc->n_scale;
-  P->flags = desc->flags;
+  P->n_scale = d->n_scale;
+  P->flags = d->flags;
+  int rc;
   try {
-    const uint32_t n_group = desc->grp_off[desc->n_out];
-    if ((desc->flags & FIONA_PLAN_CHECK_INPUTS) && n_group)
-      P->signs.assign(desc->mem_sign, desc->mem_sign + desc->grp_mem_off[n_group]);
-    rc = compile_plan(P, desc);
+    rc = compile_plan(P, d);
+    if (rc == FIONA_OK && slot_map)
+      for (auto &m : P->members) m.y = (*slot_map)[m.y];
   } catch (...) {
     rc = FIONA_ERR_NOMEM;
   }
@@ -835,6 +863,7 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
     delete P;
     return rc;
   }
+  P->n_member_desc = n_member;
   P->tiles = (ctx->N + fiona::kTile - 1) / fiona::kTile;
   P->grid = P->tiles * ctx->L;
   P->lds_bytes = (P->n_in + P->n_part + P->n_mat + P->n_seg_slots + 1 + P->obuf_rows) * kSlotBytes;
@@ -846,6 +875,7 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   P->st.output_buffer_rows = P->obuf_rows;
   P->st.lds_bytes = P->lds_bytes;
   P->st.grid = P->grid;
+  P->st.input_passes = 1;
   KShape &k = P->shape;
   k.N = ctx->N;
   k.L = ctx->L;
@@ -859,7 +889,7 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   k.n_levels = P->n_levels;
   for (uint32_t l = 0; l < fiona::kMaxLevels; ++l) k.level_end[l] = P->part_levels[l];
   k.tiles = P->tiles;
-  if (!(desc->flags & FIONA_PLAN_HOST_ONLY)) {
+  if (!(d->flags & FIONA_PLAN_HOST_ONLY)) {
     rc = upload_plan(P);
     if (rc != FIONA_OK) {
       fiona_plan_destroy(P);
@@ -870,8 +900,152 @@ int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_
   return FIONA_OK;
 }
 
+// The passes of a layer with more inputs than one tile's LDS holds: the
+// inputs are cut into consecutive ranges of at most kPassInputs, and pass g
+// takes the raw terms and the group members whose input falls in its range.
+// A group whose members span several ranges becomes one sub-sum per range,
+// each with the group's scale (exact: c (U1 + U2) = c U1 + c U2).
+int build_passes(const fiona_ctx *ctx, const fiona_layer_desc *d, uint64_t pitch, fiona_plan *P) {
+  const uint32_t n_pass = (d->n_in + kPassInputs - 1) / kPassInputs;
+  const uint32_t per = (d->n_in + n_pass - 1) / n_pass;
+  const uint32_t n_group = d->grp_off[d->n_out];
+  const uint32_t n_member = n_group ? d->grp_mem_off[n_group] : 0;
+  fiona_plan_stats_t &st = P->st;
+  for (uint32_t g = 0; g < n_pass; ++g) {
+    const uint32_t i0 = g * per, i1 = std::min(d->n_in, i0 + per);
+    std::vector<uint32_t> pm_off(d->n_out + 1, 0), pm_input, pm_pt, grp_off(d->n_out + 1, 0), grp_mem_off(1, 0),
+        mem_input, grp_scale, slot_map;
+    std::vector<int8_t> mem_sign;
+    for (uint32_t j = 0; j < d->n_out; ++j) {
+      for (uint32_t t = d->pm_off[j]; t < d->pm_off[j + 1]; ++t)
+        if (d->pm_input[t] >= i0 && d->pm_input[t] < i1) {
+          pm_input.push_back(d->pm_input[t] - i0);
+          pm_pt.push_back(d->pm_pt[t]);
+        }
+      pm_off[j + 1] = (uint32_t)pm_input.size();
+      for (uint32_t q = d->grp_off[j]; q < d->grp_off[j + 1]; ++q) {
+        const size_t before = mem_input.size();
+        for (uint32_t m = d->grp_mem_off[q]; m < d->grp_mem_off[q + 1]; ++m)
+          if (d->mem_input[m] >= i0 && d->mem_input[m] < i1) {
+            mem_input.push_back(d->mem_input[m] - i0);
+            mem_sign.push_back(d->mem_sign[m]);
+            slot_map.push_back(m);
+          }
+        if (mem_input.size() > before) {
+          grp_mem_off.push_back((uint32_t)mem_input.size());
+          grp_scale.push_back(d->grp_scale[q]);
+        }
+      }
+      grp_off[j + 1] = (uint32_t)grp_scale.size();
+    }
+    fiona_layer_desc sd = *d;
+    sd.n_in = i1 - i0;
+    sd.pm_off = pm_off.data();
+    sd.pm_input = pm_input.data();
+    sd.pm_pt = pm_pt.data();
+    sd.grp_off = grp_off.data();
+    sd.grp_mem_off = grp_mem_off.data();
+    sd.mem_input = mem_input.data();
+    sd.mem_sign = mem_sign.data();
+    sd.grp_scale = grp_scale.data();
+    sd.flags = d->flags & ~FIONA_PLAN_CHECK_INPUTS;
+    sd.pt_pitch = pitch;
+    fiona_plan *S = nullptr;
+    const int rc = build_plan(ctx, &sd, pitch, &slot_map, n_member, &S);
+    if (rc != FIONA_OK) return rc;
+    S->in_base = i0;
+    S->accumulate = g > 0;
+    P->passes.push_back(S);
+    // counts add up over the passes; the launch shape is the widest pass's
+    const fiona_plan_stats_t &a = S->st;
+    st.ct_terms += a.ct_terms;
+    st.n_pmult += a.n_pmult;
+    st.n_member += a.n_member;
+    st.n_member_nonzero += a.n_member_nonzero;
+    st.n_use += a.n_use;
+    st.n_sum_distinct += a.n_sum_distinct;
+    st.n_sum_resident += a.n_sum_resident;
+    st.pmult_per_contribution += a.pmult_per_contribution;
+    st.pmult_grouped += a.pmult_grouped;
+    st.addsub_unshared += a.addsub_unshared;
+    st.addsub_shared += a.addsub_shared;
+    st.addsub_partial += a.addsub_partial;
+    st.tile = a.tile;
+    st.waves = std::max(st.waves, a.waves);
+    st.lds_bytes = std::max(st.lds_bytes, a.lds_bytes);
+    st.grid = a.grid;
+    st.split_outputs += a.split_outputs;
+    st.segment_slots = std::max(st.segment_slots, a.segment_slots);
+    st.n_partial += a.n_partial;
+    st.partial_levels = std::max(st.partial_levels, a.partial_levels);
+    st.output_rounds = std::max(st.output_rounds, a.output_rounds);
+    st.output_buffer_rows = std::max(st.output_buffer_rows, a.output_buffer_rows);
+    P->any_signed = P->any_signed || S->any_signed;
+    P->any_raw = P->any_raw || S->any_raw;
+    P->device = S->device;
+  }
+  st.input_passes = n_pass;
+  return FIONA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fiona_plan_create(const fiona_ctx *ctx, const fiona_layer_desc *desc, fiona_plan **out) {
+  if (!out) return FIONA_ERR_ARG;
+  *out = nullptr;
+  if (!ctx || !desc) return FIONA_ERR_ARG;
+  int rc = validate_desc(desc);
+  if (rc != FIONA_OK) return rc;
+  if (desc->n_in > FIONA_MAX_LAYER_INPUTS) return FIONA_ERR_UNSUPPORTED;
+  const uint64_t ln = (uint64_t)ctx->L * ctx->N;
+  const uint64_t pitch = desc->pt_pitch ? desc->pt_pitch : ln;
+  if (pitch < ln || pitch > (1ull << 45)) return FIONA_ERR_ARG;
+  // raw-term records hold 48-bit byte offsets into the plaintext table
+  if (((uint64_t)desc->n_pt * pitch) * 8 > (1ull << 48)) return FIONA_ERR_UNSUPPORTED;
+  const uint32_t n_group = desc->grp_off[desc->n_out];
+  const uint32_t n_member = n_group ? desc->grp_mem_off[n_group] : 0;
+  fiona_plan *P = nullptr;
+  if (desc->n_in <= FIONA_MAX_INPUTS) {
+    rc = build_plan(ctx, desc, pitch, nullptr, n_member, &P);
+    if (rc != FIONA_OK) return rc;
+  } else {
+    P = new (std::nothrow) fiona_plan;
+    if (!P) return FIONA_ERR_NOMEM;
+    P->ctx = ctx;
+    P->n_in = desc->n_in;
+    P->n_out = desc->n_out;
+    P->n_pt = desc->n_pt;
+    P->pt_pitch = pitch;
+    P->n_scale = desc->n_scale;
+    P->flags = desc->flags;
+    P->n_member_desc = n_member;
+    try {
+      rc = build_passes(ctx, desc, pitch, P);
+    } catch (...) {
+      rc = FIONA_ERR_NOMEM;
+    }
+    if (rc != FIONA_OK) {
+      fiona_plan_destroy(P);
+      return rc;
+    }
+  }
+  if ((desc->flags & FIONA_PLAN_CHECK_INPUTS) && n_member) {
+    try {
+      P->signs.assign(desc->mem_sign, desc->mem_sign + n_member);
+    } catch (...) {
+      fiona_plan_destroy(P);
+      return FIONA_ERR_NOMEM;
+    }
+  }
+  *out = P;
+  return FIONA_OK;
+}
+
 void fiona_plan_destroy(fiona_plan *plan) {
   if (!plan) return;
+  for (fiona_plan *S : plan->passes) fiona_plan_destroy(S);
   if (plan->dev) (void)hipFree(plan->dev);
   delete plan;
 }
@@ -924,7 +1098,7 @@ int fiona_hybrid_linear(const fiona_plan *plan, const uint64_t *in_cts, const ui
     }
     if (rc != FIONA_OK) return rc;
   }
-  return enqueue_layer(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, plan->d_words, b, stream);
+  return enqueue_layer(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, nullptr, b, stream);
 }
 
 int fiona_hybrid_linear_static(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *pt_diags,
@@ -934,7 +1108,9 @@ int fiona_hybrid_linear_static(const fiona_plan *plan, const uint64_t *in_cts, c
   int rc = check_call(plan, in_cts, pt_diags, ternary_groups, scales, out_cts, b);
   if (rc != FIONA_OK || plan->n_out == 0) return rc;
   if (plan->flags & FIONA_PLAN_CHECK_INPUTS) return FIONA_ERR_ARG;   // its check copies into host memory
-  if (plan->blocks.size() * fiona::kSumWords * sizeof(uint32_t) > kScratchBytes) return FIONA_ERR_UNSUPPORTED;
+  size_t blocks = plan->blocks.size();
+  for (const fiona_plan *S : plan->passes) blocks = std::max(blocks, S->blocks.size());
+  if (blocks * fiona::kSumWords * sizeof(uint32_t) > kScratchBytes) return FIONA_ERR_UNSUPPORTED;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return FIONA_ERR_HIP;
   uint32_t *words = nullptr;

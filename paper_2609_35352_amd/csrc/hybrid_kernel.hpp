@@ -14,7 +14,8 @@
 //      output, or one segment of a long output: its raw terms stream their
 //      plaintext slices from HBM (each plaintext word feeds the products with
 //      both ciphertext polynomials, two batches of loads in flight) and its
-//      signed sums are read from LDS or formed in place and multiplied once by
+//      signed sums, formed between the raw batches while their loads are in
+//      flight, are read from LDS or formed in place and multiplied once by
 //      the group's scale (Sec. 4.2 "Grouping Reconstruction Operations").  Raw
 //      and signed results share one exact accumulator ("Combining the Signed
 //      and Raw Routes"), reduced once to a canonical residue.  A whole output
@@ -222,10 +223,13 @@ __device__ __forceinline__ const uint32_t *sload_block(const uint2 *pm, uint32_t
 }
 
 // All batches of the chunk block blk (uniform address), records in SGPRs:
-// batch b+1 is in flight while batch b is multiplied.  pt_end: the end of
-// the plaintext table.
+// batch b+1 is in flight while batch b is multiplied, and fill() (signed-
+// route work, which reads no HBM) runs before each batch is multiplied, so
+// that the batch's plaintext loads have longer to arrive.  pt_end: the end
+// of the plaintext table.
+template <typename Fill>
 __device__ __forceinline__ void raw_chunk(const uint32_t *blk, const char *pt_tile, const void *pt_end, uint32_t voff,
-                                          Acc &a0, Acc &a1, const uint4 *lds, uint32_t lane16) {
+                                          Acc &a0, Acc &a1, const uint4 *lds, uint32_t lane16, Fill &&fill) {
   const uint32_t hlo = sload1(blk + kChunkSlots - 1), hhi = sload1(blk + 2 * kChunkSlots - 1);
   const uint32_t nb = hhi >> 16;
   const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(pt_tile + pair64(hlo, hhi & 0xFFFFu), pt_end);
@@ -234,15 +238,20 @@ __device__ __forceinline__ void raw_chunk(const uint32_t *blk, const char *pt_ti
   uint32_t b = 0;
   for (; b + 2 < nb; b += 2) {   // batch b is in flight in wa
     raw_issue_s(wb, rs, batch_offsets(blk, b + 1), voff);
+    fill();
     raw_consume_s(a0, a1, wa, batch_rows(blk, b), lds, lane16);
     raw_issue_s(wa, rs, batch_offsets(blk, b + 2), voff);
+    fill();
     raw_consume_s(a0, a1, wb, batch_rows(blk, b + 1), lds, lane16);
   }
   if (b + 1 < nb) {   // two batches left, the first in flight in wa
     raw_issue_s(wb, rs, batch_offsets(blk, b + 1), voff);
+    fill();
     raw_consume_s(a0, a1, wa, batch_rows(blk, b), lds, lane16);
+    fill();
     raw_consume_s(a0, a1, wb, batch_rows(blk, b + 1), lds, lane16);
   } else {
+    fill();
     raw_consume_s(a0, a1, wa, batch_rows(blk, b), lds, lane16);
   }
 }
@@ -252,9 +261,19 @@ __device__ __forceinline__ void raw_chunk(const uint32_t *blk, const char *pt_ti
 // out_end = the end of the output array.  Nontemporal buffer stores
 // (measured faster than default-policy stores by 13% on a VGG11-sized layer,
 // and than device-scope ones by 2%).
+// ADD (a later input pass): y += the stored output, mod q.
+template <bool ADD>
 __device__ __forceinline__ void store_out(uint64_t *row, const void *out_end, uint32_t lane_bytes, uint32_t poly_bytes,
-                                          uint64_t y0, uint64_t y1) {
+                                          uint64_t y0, uint64_t y1, uint64_t q) {
   const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(row, out_end);
+  if constexpr (ADD) {
+    const u32x2 o0 = __builtin_amdgcn_raw_buffer_load_b64(rs, lane_bytes, 0, 0);
+    const u32x2 o1 = __builtin_amdgcn_raw_buffer_load_b64(rs, lane_bytes + poly_bytes, 0, 0);
+    y0 += pair64(o0.x, o0.y);
+    y1 += pair64(o1.x, o1.y);
+    if (y0 >= q) y0 -= q;
+    if (y1 >= q) y1 -= q;
+  }
   __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y0, (uint32_t)(y0 >> 32)}, rs, lane_bytes, 0, kStoreNT);
   __builtin_amdgcn_raw_buffer_store_b64((u32x2){(uint32_t)y1, (uint32_t)(y1 >> 32)}, rs, lane_bytes + poly_bytes, 0,
                                         kStoreNT);
@@ -282,7 +301,8 @@ struct KPlan {
 };
 
 // pt_end, out_end: the ends of the plaintext table and of the output array.
-template <int NW>
+// ADD: a later pass over an input range, which adds its sums to the outputs.
+template <int NW, bool ADD>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4, 4))) hybrid_linear_kernel(
     const uint64_t *__restrict__ in, const uint64_t *__restrict__ pt, uint64_t *__restrict__ out, const KPlan K,
     const KShape S, const void *pt_end, const void *out_end) {
@@ -356,20 +376,11 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
     acc_zero(a1);
     uint64_t r0 = 0, r1 = 0;
 
-    // raw route: one PMult per term, chunk by chunk; within a chunk batch b+1
-    // is in flight while batch b is multiplied
-    for (uint32_t c = 0; c < item.y; ++c) {
-      if (c) {
-        if (c % kFoldChunks == 0) fold(a0, a1, r0, r1, lc);   // keep the accumulators exact
-        else { carry(a0); carry(a1); }
-      }
-      raw_chunk(sload_block(pm, item.x + c), pt_tile, pt_end, voff, a0, a1, lds, lane16);
-    }
-
     // signed route: each use applies its group's scale once to a signed sum,
     // read from LDS (a resident sum) or formed in place from the use's block
     const uint32_t *ub = words + (size_t)(S.use_block0 + item.z) * kSumWords;
-    for (uint32_t u = 0; u < item.w; ++u) {
+    uint32_t u = 0;
+    auto use_one = [&]() {
       if (u && u % kFoldUses == 0) fold(a0, a1, r0, r1, lc);
       const uint32_t *blk = ub + (size_t)u * kSumWords;
       const u32x4 hd = sload4(blk);   // row counts, resident slot or kInlineSum, signed scale
@@ -377,7 +388,28 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
       const int32_t c = (int32_t)hd.z;
       smac(a0, c, (int32_t)U.x, (int32_t)U.y);
       smac(a1, c, (int32_t)U.z, (int32_t)U.w);
+      ++u;
+    };
+    // raw route: one PMult per term, chunk by chunk; within a chunk batch b+1
+    // is in flight while batch b is multiplied.  The uses are spread over the
+    // batches (per of them before each batch is multiplied; the rest after
+    // the last chunk): a wavefront then keeps plaintext loads in flight while
+    // it forms signed sums.  Measured against all uses after the raw route
+    // (in-process A/B, both load orders): VGG11 +4%, BERT +1%, Large +2-3%,
+    // ViT within the order spread.  The exact sum allows any order; chunks
+    // and uses keep their own fold counts (A0..A3 and s0, s1 bounds).
+    const uint32_t per = item.y ? (item.w + item.y * kRawBatches - 1) / (item.y * kRawBatches) : 0;
+    auto fill = [&]() {
+      for (uint32_t k = 0; k < per && u < item.w; ++k) use_one();
+    };
+    for (uint32_t c = 0; c < item.y; ++c) {
+      if (c) {
+        if (c % kFoldChunks == 0) fold(a0, a1, r0, r1, lc);   // keep the accumulators exact
+        else { carry(a0); carry(a1); }
+      }
+      raw_chunk(sload_block(pm, item.x + c), pt_tile, pt_end, voff, a0, a1, lds, lane16, fill);
     }
+    while (u < item.w) use_one();
 
     const uint64_t y0 = finish(a0, r0, lc);
     const uint64_t y1 = finish(a1, r1, lc);
@@ -389,7 +421,7 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
       obuf[(d & ~kBufferFlag) * kTile + lane] =
           make_uint4((uint32_t)y0, (uint32_t)(y0 >> 32), (uint32_t)y1, (uint32_t)(y1 >> 32));
     } else if (k < S.N) {
-      store_out(out + (size_t)d * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), y0, y1);
+      store_out<ADD>(out + (size_t)d * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), y0, y1, lc.q);
     }
   }
 
@@ -408,13 +440,14 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4,
       }
       y0 = reduce_i64((int64_t)y0, lc.q, lc.qinv);
       y1 = reduce_i64((int64_t)y1, lc.q, lc.qinv);
-      if (k < S.N) store_out(out + (size_t)sp.x * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), y0, y1);
+      if (k < S.N) store_out<ADD>(out + (size_t)sp.x * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), y0, y1, lc.q);
     }
     for (uint32_t e = wave; e < rr.y; e += NW) {
       const uint4 v = obuf[e * kTile + lane];
       const uint32_t j = K.flush[rr.x + e];
       if (k < S.N)
-        store_out(out + (size_t)j * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), pair64(v.x, v.y), pair64(v.z, v.w));
+        store_out<ADD>(out + (size_t)j * 2 * LN + out_row, out_end, lane * 8u, (uint32_t)(LN * 8), pair64(v.x, v.y),
+                       pair64(v.z, v.w), lc.q);
     }
     if (rd + 1 < S.n_rounds) __syncthreads();   // the next round refills the buffer
   }

@@ -94,7 +94,7 @@ def test_plan_validation_errors():
     with pytest.raises(fiona.FionaError) as e:
         fiona.Plan(ctx, flags=HOST, **a)
     assert e.value.status == -1
-    a = dict(ok); a["n_in"] = 160
+    a = dict(ok); a["n_in"] = 65537   # beyond FIONA_MAX_LAYER_INPUTS
     with pytest.raises(fiona.FionaError) as e:
         fiona.Plan(ctx, flags=HOST, **a)
     assert e.value.status == -3
@@ -375,3 +375,25 @@ def test_checking_plan_preconditions_on_the_host():
     # a plan made without the flag keeps no signs
     plain = fiona.Plan.from_layer(ctx, layer, flags=HOST)
     assert ok(plain, layer.mem_sign, layer.scales) == fiona.FIONA_ERR_ARG
+
+
+@pytest.mark.parametrize("n_in,passes", [(159, 1), (160, 2), (256, 2), (320, 3), (1000, 8)])
+def test_input_passes(n_in, passes):
+    """Layers with more inputs than one tile's LDS holds run in passes over
+    input ranges of at most 128; every raw term and member lands in exactly
+    one pass, and a group spanning ranges becomes one use per range."""
+    cfg = synth.LayerConfig("wide", N=64, L=1, n_in=n_in, n_out=5, T=-(-2 * n_in // 16) * 16, g=16, ternary=0.6, pool=3)
+    lay = synth.make_layer(cfg, 2, moduli=synth.ntt_primes(64, 1))
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    st = fiona.Plan.from_layer(ctx, lay, flags=HOST).stats()
+    assert st["input_passes"] == passes
+    assert st["ct_terms"] == lay.ct_terms and st["n_pmult"] == lay.n_pm and st["n_member"] == lay.n_member
+    assert st["lds_bytes"] <= 160 * 1024
+    per = -(-n_in // passes)
+    # uses: every group once per input range its nonzero members touch
+    uses = 0
+    for q in range(lay.n_group):
+        m0, m1 = int(lay.grp_mem_off[q]), int(lay.grp_mem_off[q + 1])
+        nz = lay.mem_input[m0:m1][lay.mem_sign[m0:m1] != 0]
+        uses += len(set(int(i) // per for i in nz))
+    assert st["n_use"] == uses

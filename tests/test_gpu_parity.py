@@ -108,6 +108,12 @@ SMALL = {
     "repeated_pool": synth.LayerConfig("repeated_pool", N=256, L=2, n_in=6, n_out=48, T=80, g=10, ternary=0.9,
                                        pool=4),
     "repeated_iid": synth.LayerConfig("repeated_iid", N=256, L=2, n_in=7, n_out=48, T=160, g=20, ternary=0.9),
+    # more inputs than one tile's LDS holds: passes over input ranges, groups crossing them
+    "wide_320": synth.LayerConfig("wide_320", N=256, L=2, n_in=320, n_out=6, T=640, g=16, ternary=0.6, pool=3),
+    "wide_160_bursts": synth.LayerConfig("wide_160_bursts", N=128, L=2, n_in=160, n_out=40, T=320, g=16,
+                                         ternary=0.5),
+    "wide_partial": synth.LayerConfig("wide_partial", N=128, L=2, n_in=200, n_out=48, T=400, g=40, ternary=0.95),
+    "wide_repeat": synth.LayerConfig("wide_repeat", N=96, L=2, n_in=170, n_out=8, T=800, g=200, ternary=0.5),
 }
 
 
@@ -160,7 +166,10 @@ def test_small_layer_elementwise(dev, name):
                                         ("partial_share", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
                                         ("fold_raw", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
                                         ("repeated_pool", fiona.FIONA_PLAN_NO_LDS_SUMS),
-                                        ("repeated_pool", fiona.FIONA_PLAN_NO_PARTIAL_SHARING)])
+                                        ("repeated_pool", fiona.FIONA_PLAN_NO_PARTIAL_SHARING),
+                                        ("wide_partial", fiona.FIONA_PLAN_NO_LDS_SUMS),
+                                        ("wide_160_bursts", fiona.FIONA_PLAN_NO_OUTPUT_BURSTS),
+                                        ("wide_320", fiona.FIONA_PLAN_PER_CONTRIBUTION)])
 def test_plan_variants_agree(dev, name, flags):
     layer = _small_layer(name)
     x, pt = synth.input_values(layer), synth.pt_values(layer)
@@ -569,3 +578,21 @@ def test_checking_plan(dev):
     assert e.value.status == fiona.FIONA_ERR_PRECONDITION
     torch.cuda.synchronize()
     assert bool((out2 == -1).all())
+
+
+def test_checking_plan_input_passes(dev):
+    """A checking plan over several input passes: the same outputs, and a
+    changed sign of a member in the second pass's range is refused."""
+    import torch
+    layer = _small_layer("wide_320")
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    out_t, in_t, pt_t, plan = _run(layer, dev, x, pt, flags=fiona.FIONA_PLAN_CHECK_INPUTS)
+    assert plan.stats()["input_passes"] == 3
+    _assert_equal(_host(out_t, layer), oracle.weighted_sum_layer(layer, x, pt, n_threads=8), "checking plan, passes")
+    signs2 = layer.mem_sign.copy()
+    k = int(np.nonzero((layer.mem_input >= 150) & (signs2 != 0))[0][0])
+    signs2[k] = -signs2[k]
+    with pytest.raises(fiona.FionaError) as e:
+        fiona.hybrid_linear(plan, in_t, pt_t, _to_dev(signs2, np.int8, dev), _to_dev(layer.scales, np.int64, dev),
+                            torch.empty_like(out_t))
+    assert e.value.status == fiona.FIONA_ERR_PRECONDITION

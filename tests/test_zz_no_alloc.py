@@ -89,3 +89,14 @@ def test_static_entry_point_limits():
         fiona.hybrid_linear_static(chk, _t(x, np.int64, dev), _t(pt, np.int64, dev),
                                    _t(small.mem_sign, np.int8, dev), _t(small.scales, np.int64, dev), out2)
     assert e.value.status == fiona.FIONA_ERR_ARG
+
+
+def test_static_entry_point_input_passes():
+    """A layer over several input passes: every pass's word blocks go to the
+    same static array in turn on the stream."""
+    dev = _dev()
+    wide = synth.make_layer(synth.LayerConfig("static_wide", N=128, L=2, n_in=200, n_out=12, T=400, g=16,
+                                              ternary=0.6), 6, moduli=synth.ntt_primes(128, 2))
+    r, g, e, plan = _both(wide, dev)
+    assert plan.stats()["input_passes"] == 2
+    assert np.array_equal(r, e) and np.array_equal(g, r)
