@@ -787,7 +787,6 @@ int enqueue_one(const fiona_plan *plan, const uint64_t *in_cts, const uint64_t *
     pp.words = words;
     pp.scales = scales;
     pp.n_blocks = n_blocks;
-    pp.zero_row = plan->shape.zero_row;
     hipLaunchKernelGGL(fiona::pack_members_kernel, dim3((n_blocks + 3) / 4), dim3(256), 0, stream, pp);
     if (hipGetLastError() != hipSuccess) return FIONA_ERR_HIP;
   }
