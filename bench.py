@@ -443,7 +443,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--rounds", type=int, default=2, help="rounds of hybrid then all-PMult per layer")
-    ap.add_argument("--layers", default=",".join(LAYERS), help="comma-separated layers to time")
+    ap.add_argument("--layers", default=",".join(LAYERS),
+                    help="comma-separated layers to time ('none': only the --ablation/--rescale/--rotate steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streams", action="store_true", help="skip the read and copy ceilings")
     ap.add_argument("--seed", type=int, default=1)
@@ -489,10 +490,12 @@ def main():
     dev = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=dev)   # default priority
     pad_mode = False if args.packed_pts else (True if args.pt_pad is None else args.pt_pad)
-    names = [n for n in args.layers.split(",") if n]
+    names = [n for n in args.layers.split(",") if n and n != "none"]
     for n in names:
         if n not in synth.CONFIGS:
             raise SystemExit("unknown layer %s" % n)
+    if not names and not (args.ablation or args.rescale or args.rotate):
+        raise SystemExit("nothing to time: --layers none needs --ablation, --rescale or --rotate")
 
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
@@ -500,7 +503,7 @@ def main():
     for n in names:
         log("[bench] %s: %s" % (n, synth.CONFIGS[n].description))
         records.append(time_layer(n, dev, stream, args.steps, args.warmup, args.rounds, args.seed, pad_mode))
-    head = next((r for r in records if r["layer"] == "large4096"), records[-1])
+    head = next((r for r in records if r["layer"] == "large4096"), records[-1] if records else None)
 
     extra = {}
     if args.ablation or args.rescale or args.rotate:
@@ -535,6 +538,9 @@ def main():
         r["mac_rate_frac"] = round(w / mb["words_per_s"], 4)
     streams = None if args.no_streams else time_streams(stream)
     wall = time.perf_counter() - t_wall0
+    if head is None:   # --layers none: the extra steps only
+        print(json.dumps(dict(extra, mac_microbench=mb, streams=streams, gpu_wall_s=round(wall, 2))), flush=True)
+        return
 
     hy = head["hybrid"]
     result = {

@@ -173,7 +173,8 @@ uint64_t fiona_pt_pitch_hint(const fiona_ctx *ctx);
  *     group spanning several ranges becomes one sub-sum per range with the
  *     group's scale, exact since c*(U1 + U2) = c*U1 + c*U2); the first pass
  *     stores the outputs and each later pass adds its sums to them mod q_l,
- *     so the outputs are read and written once more per extra pass;
+ *     so the outputs are read and written once more per extra pass; a range
+ *     that no term reads gets no pass;
  * The plan keeps a reference to ctx (which must outlive it).  Errors:
  * FIONA_ERR_ARG (also a pt_pitch below L*N), FIONA_ERR_PLAN, FIONA_ERR_UNSUPPORTED
  * (more than FIONA_MAX_LAYER_INPUTS inputs, or a plaintext table beyond 2^48 bytes), FIONA_ERR_NOMEM, FIONA_ERR_HIP.

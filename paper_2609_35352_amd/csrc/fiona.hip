@@ -937,6 +937,9 @@ int build_passes(const fiona_ctx *ctx, const fiona_layer_desc *d, uint64_t pitch
       }
       grp_off[j + 1] = (uint32_t)grp_scale.size();
     }
+    // a range that no term reads adds nothing: no pass (unless every range
+    // is empty, when the first pass still writes the zero outputs)
+    if (pm_input.empty() && grp_scale.empty() && (g + 1 < n_pass || !P->passes.empty())) continue;
     fiona_layer_desc sd = *d;
     sd.n_in = i1 - i0;
     sd.pm_off = pm_off.data();
@@ -953,7 +956,7 @@ int build_passes(const fiona_ctx *ctx, const fiona_layer_desc *d, uint64_t pitch
     const int rc = build_plan(ctx, &sd, pitch, &slot_map, n_member, &S);
     if (rc != FIONA_OK) return rc;
     S->in_base = i0;
-    S->accumulate = g > 0;
+    S->accumulate = !P->passes.empty();
     P->passes.push_back(S);
     // counts add up over the passes; the launch shape is the widest pass's
     const fiona_plan_stats_t &a = S->st;
@@ -983,7 +986,7 @@ int build_passes(const fiona_ctx *ctx, const fiona_layer_desc *d, uint64_t pitch
     P->any_raw = P->any_raw || S->any_raw;
     P->device = S->device;
   }
-  st.input_passes = n_pass;
+  st.input_passes = (uint32_t)P->passes.size();
   return FIONA_OK;
 }
 

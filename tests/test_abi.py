@@ -397,3 +397,13 @@ def test_input_passes(n_in, passes):
         nz = lay.mem_input[m0:m1][lay.mem_sign[m0:m1] != 0]
         uses += len(set(int(i) // per for i in nz))
     assert st["n_use"] == uses
+
+
+def test_input_passes_skip_unread_ranges():
+    """Input ranges that no term reads get no pass (320 inputs, terms on the
+    first 64 only: one pass)."""
+    cfg = synth.LayerConfig("wide_sparse", N=100, L=2, n_in=320, n_out=5, T=64, g=8, ternary=0.5)
+    lay = synth.make_layer(cfg, 5, moduli=synth.ntt_primes(128, 2))
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    st = fiona.Plan.from_layer(ctx, lay, flags=HOST).stats()
+    assert st["input_passes"] == 1 and st["ct_terms"] == lay.ct_terms

@@ -114,6 +114,8 @@ SMALL = {
                                          ternary=0.5),
     "wide_partial": synth.LayerConfig("wide_partial", N=128, L=2, n_in=200, n_out=48, T=400, g=40, ternary=0.95),
     "wide_repeat": synth.LayerConfig("wide_repeat", N=96, L=2, n_in=170, n_out=8, T=800, g=200, ternary=0.5),
+    # ragged N; the second and third input passes hold no term (their launches store each output + 0)
+    "wide_sparse": synth.LayerConfig("wide_sparse", N=100, L=2, n_in=320, n_out=5, T=64, g=8, ternary=0.5),
 }
 
 
@@ -596,3 +598,20 @@ def test_checking_plan_input_passes(dev):
         fiona.hybrid_linear(plan, in_t, pt_t, _to_dev(signs2, np.int8, dev), _to_dev(layer.scales, np.int64, dev),
                             torch.empty_like(out_t))
     assert e.value.status == fiona.FIONA_ERR_PRECONDITION
+
+
+def test_input_pass_gap(dev):
+    """320 inputs, terms on inputs 0..59 and 260..319 only: the middle input
+    range gets no pass, and the last pass adds to the first one's outputs."""
+    base = synth.make_layer(synth.LayerConfig("gap", N=192, L=2, n_in=120, n_out=6, T=240, g=12, ternary=0.6, pool=3),
+                            7, moduli=synth.ntt_primes(256, 2))
+    remap = lambda a: np.where(a < 60, a, a + 200).astype(np.uint32)
+    layer = synth.Layer(**{**base.__dict__, "n_in": 320, "pm_input": remap(base.pm_input),
+                           "mem_input": remap(base.mem_input)})
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    st = fiona.Plan.from_layer(ctx, layer, flags=fiona.FIONA_PLAN_HOST_ONLY).stats()
+    assert st["input_passes"] == 2
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    out_t, *_ = _run(layer, dev, x, pt)
+    _assert_equal(_host(out_t, layer), expect, "input pass gap")
