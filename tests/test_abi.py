@@ -8,6 +8,7 @@ import re
 import numpy as np
 import pytest
 
+import random_layers
 import synth
 import paper_2609_35352_amd as fiona
 
@@ -407,3 +408,22 @@ def test_input_passes_skip_unread_ranges():
     ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
     st = fiona.Plan.from_layer(ctx, lay, flags=HOST).stats()
     assert st["input_passes"] == 1 and st["ct_terms"] == lay.ct_terms
+
+
+@pytest.mark.parametrize("seed", range(64))
+def test_random_layer_plans(seed):
+    """Random layer descriptions (random_layers.py) compile on the host under
+    their flags; the counts match the description and the launch fits."""
+    lay = random_layers.random_layer(seed)
+    flags, _ = random_layers.random_flags(seed)
+    ctx = fiona.Ctx(lay.N, lay.L, lay.moduli)
+    st = fiona.Plan.from_layer(ctx, lay, flags=HOST | flags).stats()
+    assert st["ct_terms"] == lay.ct_terms and st["n_pmult"] == lay.n_pm and st["n_member"] == lay.n_member
+    nz = int(np.count_nonzero(lay.mem_sign))
+    assert st["n_member_nonzero"] == nz and st["pmult_per_contribution"] == lay.n_pm + nz
+    assert 1 <= st["input_passes"] <= max(1, -(-lay.n_in // 128))
+    if lay.n_in <= 159:   # FIONA_MAX_INPUTS: one tile of every input in LDS
+        assert st["input_passes"] == 1
+    assert st["lds_bytes"] <= 160 * 1024 and st["waves"] in (8, 16)
+    if flags & fiona.FIONA_PLAN_PER_CONTRIBUTION:
+        assert st["pmult_grouped"] == st["pmult_per_contribution"]

@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
+import random_layers
 import synth
 import paper_2609_35352_amd as fiona
 
@@ -114,7 +115,7 @@ SMALL = {
                                          ternary=0.5),
     "wide_partial": synth.LayerConfig("wide_partial", N=128, L=2, n_in=200, n_out=48, T=400, g=40, ternary=0.95),
     "wide_repeat": synth.LayerConfig("wide_repeat", N=96, L=2, n_in=170, n_out=8, T=800, g=200, ternary=0.5),
-    # ragged N; the second and third input passes hold no term (their launches store each output + 0)
+    # ragged N; 320 inputs, terms on the first 64 only: the other input ranges get no pass
     "wide_sparse": synth.LayerConfig("wide_sparse", N=100, L=2, n_in=320, n_out=5, T=64, g=8, ternary=0.5),
 }
 
@@ -615,3 +616,19 @@ def test_input_pass_gap(dev):
     expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
     out_t, *_ = _run(layer, dev, x, pt)
     _assert_equal(_host(out_t, layer), expect, "input pass gap")
+
+
+@pytest.mark.parametrize("seed", range(64))
+def test_random_layer(dev, seed):
+    """Random layer descriptions (random terms and members, repeated inputs,
+    empty outputs and groups, shared and reversed sums, hot pairs, input
+    passes, ragged N, moduli near 2^20 and 2^50) under random plan flags and
+    plaintext pitches, element by element against the oracle."""
+    layer = random_layers.random_layer(seed)
+    flags, pitch = random_layers.random_flags(seed)
+    _say("random layer %d: N=%d L=%d n_in=%d n_out=%d raw=%d groups=%d members=%d flags=%d pitch=%s"
+         % (seed, layer.N, layer.L, layer.n_in, layer.n_out, layer.n_pm, layer.n_group, layer.n_member, flags, pitch))
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    out_t, *_ = _run(layer, dev, x, pt, flags=flags, pitch=pitch)
+    _assert_equal(_host(out_t, layer), expect, "random layer %d" % seed)
