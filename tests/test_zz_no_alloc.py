@@ -100,3 +100,36 @@ def test_static_entry_point_input_passes():
     r, g, e, plan = _both(wide, dev)
     assert plan.stats()["input_passes"] == 2
     assert np.array_equal(r, e) and np.array_equal(g, r)
+
+
+@pytest.mark.parametrize("seed", range(0, 64, 4))
+def test_static_entry_point_random_layers(seed):
+    """The random layer descriptions (random_layers.py) under their plan flags
+    (checking plans aside, which the static entry point refuses): both entry
+    points bit-identical, and equal to the oracle."""
+    import torch
+    import random_layers
+    dev = _dev()
+    layer = random_layers.random_layer(seed)
+    flags, _ = random_layers.random_flags(seed)
+    flags &= ~fiona.FIONA_PLAN_CHECK_INPUTS
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    plan = fiona.Plan.from_layer(ctx, layer, flags=flags)
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    one = lambda a, dt, t: _t(a, dt, dev) if a.size else torch.zeros(1, dtype=t, device=dev)
+    in_t, pt_t = one(x, np.int64, torch.int64), one(pt, np.int64, torch.int64)
+    sign_t, scale_t = one(layer.mem_sign, np.int8, torch.int8), one(layer.scales, np.int64, torch.int64)
+    n = layer.n_out * 2 * layer.L * layer.N
+    ref = torch.full((n,), -1, dtype=torch.int64, device=dev)
+    got = torch.full((n,), -2, dtype=torch.int64, device=dev)
+    print("[no-alloc] random layer %d: N=%d L=%d n_in=%d outputs=%d flags=%d" % (seed, layer.N, layer.L, layer.n_in,
+                                                                                   layer.n_out, flags), flush=True)
+    fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, ref)
+    fiona.hybrid_linear_static(plan, in_t, pt_t, sign_t, scale_t, got)
+    torch.cuda.synchronize()
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    r = ref.cpu().numpy().view(np.uint64).reshape(expect.shape)
+    g = got.cpu().numpy().view(np.uint64).reshape(expect.shape)
+    assert np.array_equal(r, expect), "fiona_hybrid_linear differs from the oracle"
+    bad = np.argwhere(g != r)
+    assert not bad.size, "%d words differ, first at %s" % (len(bad), tuple(bad[0]))
