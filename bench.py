@@ -329,8 +329,8 @@ def time_rescale(layer, dev, steps, warmup, stream):
 
 def host_cpu():
     """CPU model, the host's CPU count and the threads this process may use
-    (its affinity, capped by OMP_NUM_THREADS where set: a GPU machine gives one
-    GPU's job a share of its cores)."""
+    (its affinity, capped by OMP_NUM_THREADS where set: a shared multi-GPU
+    host gives each GPU's job a share of its cores)."""
     model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -464,8 +464,8 @@ def main():
                     help="only copy 4 GiB device-to-device (torch copy kernel) to calibrate HBM counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build measures one GPU only; the hybrid weighted sum has no "
-              "multi-GPU path here (run with --gpus 1)", file=sys.stderr)
+        print("bench.py: measures one GPU only; the hybrid weighted sum has no "
+              "multi-GPU path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import torch
