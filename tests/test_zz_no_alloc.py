@@ -133,3 +133,41 @@ def test_static_entry_point_random_layers(seed):
     assert np.array_equal(r, expect), "fiona_hybrid_linear differs from the oracle"
     bad = np.argwhere(g != r)
     assert not bad.size, "%d words differ, first at %s" % (len(bad), tuple(bad[0]))
+
+
+def test_entry_points_in_a_hip_graph():
+    """Both entry points captured in a HIP graph (the callers the static entry
+    point is for) and replayed three times, with eager work on the outputs
+    and a synchronisation between the replays; every replay equals the eager
+    result, which equals the oracle."""
+    import torch
+    dev = _dev()
+    layer = synth.make_layer(FIRST, 6, moduli=synth.ntt_primes(512, 3))
+    ctx = fiona.Ctx(layer.N, layer.L, layer.moduli)
+    plan = fiona.Plan.from_layer(ctx, layer)
+    x, pt = synth.input_values(layer), synth.pt_values(layer)
+    in_t, pt_t = _t(x, np.int64, dev), _t(pt, np.int64, dev)
+    sign_t, scale_t = _t(layer.mem_sign, np.int8, dev), _t(layer.scales, np.int64, dev)
+    n = layer.n_out * 2 * layer.L * layer.N
+    ref = torch.full((n,), -1, dtype=torch.int64, device=dev)
+    fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, ref)
+    torch.cuda.synchronize()
+    expect = oracle.weighted_sum_layer(layer, x, pt, n_threads=8)
+    assert np.array_equal(ref.cpu().numpy().view(np.uint64).reshape(expect.shape), expect)
+    s = torch.cuda.Stream(device=dev)
+    for name, entry in (("fiona_hybrid_linear", fiona.hybrid_linear), ("fiona_hybrid_linear_static",
+                                                                        fiona.hybrid_linear_static)):
+        out = torch.full((n,), -2, dtype=torch.int64, device=dev)
+        entry(plan, in_t, pt_t, sign_t, scale_t, out, stream=s)   # outside the graph first
+        torch.cuda.synchronize()
+        print("[no-alloc] graph capture of %s" % name, flush=True)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            entry(plan, in_t, pt_t, sign_t, scale_t, out, stream=s)
+        for r in range(3):
+            out.fill_(-3)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(out, ref), "%s: replay %d differs from the eager result" % (name, r)
+        del g
