@@ -138,3 +138,39 @@ def test_rescale_errors(dev):
     with pytest.raises(fiona.FionaError) as e:
         fiona.rescale(r, a, 1, a[8:])      # output overlaps the input
     assert e.value.status == -5
+
+
+def test_rescale_in_a_hip_graph(dev):
+    """fiona_rescale captured in a HIP graph (one call = four NTT pass
+    launches, no memset or copy) and replayed three times, with eager work on
+    the output between the replays: every replay equals the eager call, which
+    equals the oracle."""
+    import torch
+    N, L, n_ct = 1 << 12, 3, 3
+    _say("[rescale] graph capture N=%d L=%d n_ct=%d" % (N, L, n_ct))
+    moduli = synth.ntt_primes(N, L)
+    cts = _random_cts(n_ct, moduli, N, 9)
+    ctx = fiona.Ctx(N, L, moduli)
+    r = fiona.Rescaler(ctx, n_ct)
+    in_t = torch.from_numpy(cts.reshape(-1).view(np.int64)).to(dev)
+    n = n_ct * 2 * (L - 1) * N
+    ref = torch.full((n,), -1, dtype=torch.int64, device=dev)
+    fiona.rescale(r, in_t, n_ct, ref)
+    torch.cuda.synchronize()
+    got = ref.cpu().numpy().view(np.uint64).reshape(n_ct, 2, L - 1, N)
+    for c in range(n_ct):
+        assert np.array_equal(got[c], rs.rescale(cts[c], moduli))
+    s = torch.cuda.Stream(device=dev)
+    out = torch.full((n,), -2, dtype=torch.int64, device=dev)
+    fiona.rescale(r, in_t, n_ct, out, stream=s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        fiona.rescale(r, in_t, n_ct, out, stream=s)
+    for rep in range(3):
+        out.fill_(-3)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), "replay %d differs from the eager call" % rep
+    del g

@@ -258,3 +258,39 @@ def test_rotation_key_layout_format(N, g):
     src = ((i - (g - 1) // 2) * pow(g, -1, N)) % N
     np.testing.assert_array_equal(got, keys[0].reshape(-1, N)[:, src])
 
+
+
+def test_rotate_in_a_hip_graph():
+    """fiona_hoisted_rotate captured in a HIP graph (one call = its launches,
+    the Galois elements passed by value, no memset or copy) and replayed three
+    times, with eager work on the output between the replays: every replay
+    equals the eager call, which equals the oracle."""
+    dev = _dev()
+    N, L = 4096, 3
+    galois = [orot.galois_element(r, N) for r in (1, 2, 5)]
+    moduli, P, ct, keys = _random_case(N, L, len(galois), 7)
+    ref_host, rot, ctx = _run_gpu(moduli, P, ct, keys, galois, dev)
+    for r, g in enumerate(galois):
+        assert np.array_equal(ref_host[r], orot.rotate(ct, g, keys[r], moduli, P))
+    kw = rot.key_words()
+    nat = _u64(keys.reshape(len(galois), kw), dev)
+    lib_keys = torch.empty(len(galois) * kw, dtype=torch.int64, device=dev)
+    for r, g in enumerate(galois):
+        fiona.rotation_key_layout(rot, g, nat[r], lib_keys[r * kw:(r + 1) * kw])
+    ct_t = _u64(ct, dev)
+    ref = _u64(ref_host.reshape(-1), dev)
+    s = torch.cuda.Stream(device=dev)
+    out = torch.full((len(galois) * 2 * L * N,), -2, dtype=torch.int64, device=dev)
+    fiona.hoisted_rotate(rot, ct_t, galois, lib_keys, out, stream=s)
+    torch.cuda.synchronize()
+    print("[rotate] graph capture N=%d L=%d rotations=%s" % (N, L, galois), flush=True)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        fiona.hoisted_rotate(rot, ct_t, galois, lib_keys, out, stream=s)
+    for rep in range(3):
+        out.fill_(-3)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), "replay %d differs from the eager call" % rep
+    del graph
