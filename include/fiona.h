@@ -259,7 +259,9 @@ int fiona_plan_check_inputs(const fiona_plan *plan, const int8_t *signs, const u
  *                   canonical residues in [0, q_l); must not overlap any input
  *   stream          HIP stream the work is queued on (0 = legacy default)
  * Asynchronous: returns once the kernel is queued; the buffers must stay
- * valid and unchanged until the stream reaches it.  Allocates nothing.
+ * valid and unchanged until the stream reaches it.  Allocates nothing, and
+ * issues kernel launches only (no memset or copy; a checking plan excepted),
+ * so a call can be captured in a HIP graph.
  * Results are exact (bit-identical to evaluating every term on its own mod q_l).
  * Input ranges and signs above are preconditions, checked only by a checking
  * plan (FIONA_PLAN_CHECK_INPUTS).  Device pointers need 8-byte alignment
@@ -329,10 +331,11 @@ void fiona_rescaler_destroy(fiona_rescaler *rescaler);
  *   out_cts  device, [n_ct][2][L-1][N] uint64, overwritten with canonical
  *            residues; must not overlap in_cts
  *   n_ct     at most the max_ct of the rescaler
- * Asynchronous on stream; allocates nothing.  The rescaler's workspace is
- * shared by its calls: one rescaler must not be used by two streams at the
- * same time.  Errors (nothing is launched): FIONA_ERR_ARG, FIONA_ERR_ALIGN,
- * FIONA_ERR_ALIAS, FIONA_ERR_HIP.
+ * Asynchronous on stream; allocates nothing, and issues kernel launches only
+ * (no memset or copy), so a call can be captured in a HIP graph.  The
+ * rescaler's workspace is shared by its calls: one rescaler must not be used
+ * by two streams at the same time.  Errors (nothing is launched):
+ * FIONA_ERR_ARG, FIONA_ERR_ALIGN, FIONA_ERR_ALIAS, FIONA_ERR_HIP.
  */
 int fiona_rescale(const fiona_rescaler *rescaler, const uint64_t *in_cts, uint32_t n_ct, uint64_t *out_cts,
                   hipStream_t stream);
@@ -387,8 +390,10 @@ int fiona_rescale(const fiona_rescaler *rescaler, const uint64_t *in_cts, uint32
  *   out_cts  device, [n_rot][2][L][N], overwritten with canonical residues;
  *            must not overlap ct or keys
  *   n_rot    at most the rotator's max_rot
- * Asynchronous on stream; allocates nothing.  The workspace is shared by the
- * rotator's calls: one rotator must not be used by two streams at the same
+ * Asynchronous on stream; allocates nothing, and issues kernel launches only
+ * (the Galois elements travel by value in the launch arguments), so a call
+ * can be captured in a HIP graph.  The workspace is shared by the rotator's
+ * calls: one rotator must not be used by two streams at the same
  * time.  Results are exact: bit-identical to the definition above computed
  * in integers.  Errors (nothing is launched): FIONA_ERR_ARG, FIONA_ERR_ALIGN,
  * FIONA_ERR_ALIAS, FIONA_ERR_HIP.
