@@ -1,7 +1,7 @@
 """Benchmark of the hybrid weighted sum on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--rounds R] [--layers vgg11,vit768,bert_ffn,large4096]
-                    [--no-cpu-baseline] [--ablation] [--rescale] [--rotate] [--config NAME]
+                    [--no-cpu-baseline] [--ablation] [--rescale] [--rotate] [--pipeline] [--config NAME]
 
 The metric is quoted on the four N=2^16 layers, so a default run times all
 four, each both ways: the hybrid layer (PMult for raw terms, Add/Sub and one
@@ -327,6 +327,90 @@ def time_rescale(layer, dev, steps, warmup, stream):
             "butterflies_per_s": round(butterflies / (ms * 1e-3), 1)}
 
 
+def time_pipeline(layer, dev, steps, warmup, stream):
+    """One whole layer step on one stream: the n_in - 1 baby-step rotations of
+    one ciphertext, written straight into the weighted sum's input array (baby
+    step 0 is the ciphertext itself), the hybrid weighted sum, and the rescale
+    of its outputs.  Timed eagerly (HIP events between the three stages; per
+    stage and per step the median of the timed steps) and as one HIP graph of
+    the three stages replayed (the median replay).  Device-generated inputs:
+    ciphertext, keys (uniform residues in the library's layout), plaintexts.
+    Layers whose plaintexts fit one launch (one hybrid chunk)."""
+    import torch
+    import synth
+    import synth.gpu
+    import paper_2609_35352_amd as fiona
+
+    if layer.cfg.chunks_hybrid != 1:
+        raise ValueError("the pipeline times layers whose weighted sum is one launch")
+    N, L, LN = layer.N, layer.L, layer.L * layer.N
+    P = synth.ntt_primes(N, L + 1)[L]
+    galois = [pow(5, r, 2 * N) for r in range(1, layer.n_in)]
+    n = len(galois)
+    ctx = fiona.Ctx(N, L, layer.moduli)
+    rot = fiona.Rotator(ctx, P, max(n, 1))
+    kw = rot.key_words()
+    in_t = torch.empty(layer.n_in * 2 * LN, dtype=torch.int64, device=dev)
+    ct_t, rot_t = in_t[: 2 * LN], in_t[2 * LN:]
+    synth.gpu.fill_cts(layer, ct_t, 1)
+    keys_t = torch.empty(max(n, 1) * kw, dtype=torch.int64, device=dev)
+    synth.gpu.fill_rows(keys_t, max(n, 1) * kw // N, list(layer.moduli) + [P], N, layer.seed, synth.TAG_KEY)
+    pitch = ctx.pt_pitch_hint()
+    plan = fiona.Plan.from_layer(ctx, layer, pt_pitch=pitch)
+    pt_t = torch.empty((max(1, layer.n_pt) - 1) * pitch + LN, dtype=torch.int64, device=dev)
+    synth.gpu.fill_pts(layer, pt_t, pitch)
+    sign_t, scale_t = _dev_signs_scales(layer, dev)
+    out_t = torch.empty(layer.n_out * 2 * LN, dtype=torch.int64, device=dev)
+    resc = fiona.Rescaler(ctx, layer.n_out)
+    res_t = torch.empty(layer.n_out * 2 * (L - 1) * N, dtype=torch.int64, device=dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        if n:
+            fiona.hoisted_rotate(rot, ct_t, galois, keys_t, rot_t, stream=stream)
+        if ev:
+            ev[1].record(stream)
+        fiona.hybrid_linear(plan, in_t, pt_t, sign_t, scale_t, out_t, stream=stream)
+        if ev:
+            ev[2].record(stream)
+        fiona.rescale(resc, out_t, layer.n_out, res_t, stream=stream)
+        if ev:
+            ev[3].record(stream)
+
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for ev in evs:
+        step(ev)
+    torch.cuda.synchronize()
+    med = lambda a, b: float(np.median([ev[a].elapsed_time(ev[b]) for ev in evs]))
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        step()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    ge = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ge[0].record(stream)
+    with torch.cuda.stream(stream):
+        for i in range(steps):
+            graph.replay()
+            ge[i + 1].record(stream)
+    torch.cuda.synchronize()
+    g_ms = float(np.median([ge[i].elapsed_time(ge[i + 1]) for i in range(steps)]))
+    rec = {"rotations": n, "rotate_ms": round(med(0, 1), 4), "weighted_sum_ms": round(med(1, 2), 4),
+           "rescale_ms": round(med(2, 3), 4), "step_ms": round(med(0, 3), 4), "graph_step_ms": round(g_ms, 4),
+           "weighted_sum_share": round(med(1, 2) / med(0, 3), 4)}
+    log("[bench] layer step (%d rotations, weighted sum, rescale of %d outputs): %.3f ms eager "
+        "(%.3f + %.3f + %.3f), %.3f ms as one HIP graph"
+        % (n, layer.n_out, rec["step_ms"], rec["rotate_ms"], rec["weighted_sum_ms"], rec["rescale_ms"], g_ms))
+    del graph
+    return rec
+
+
 def host_cpu():
     """CPU model, the host's CPU count and the threads this process may use
     (its affinity, capped by OMP_NUM_THREADS where set: a shared multi-GPU
@@ -454,6 +538,9 @@ def main():
                          "(fiona_hoisted_rotate)")
     ap.add_argument("--rescale", action="store_true",
                     help="also time the rescale epilogue on the layer's outputs (fiona_rescale)")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="also time one whole layer step of --config: its rotations, weighted sum and rescale "
+                         "on one stream, eagerly and as one HIP graph")
     ap.add_argument("--ablation", action="store_true",
                     help="also time the layer compiled per-contribution, grouped, grouped+shared (Sec. 6.2)")
     ap.add_argument("--packed-pts", action="store_true",
@@ -494,8 +581,8 @@ def main():
     for n in names:
         if n not in synth.CONFIGS:
             raise SystemExit("unknown layer %s" % n)
-    if not names and not (args.ablation or args.rescale or args.rotate):
-        raise SystemExit("nothing to time: --layers none needs --ablation, --rescale or --rotate")
+    if not names and not (args.ablation or args.rescale or args.rotate or args.pipeline):
+        raise SystemExit("nothing to time: --layers none needs --ablation, --rescale, --rotate or --pipeline")
 
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
@@ -506,7 +593,7 @@ def main():
     head = next((r for r in records if r["layer"] == "large4096"), records[-1] if records else None)
 
     extra = {}
-    if args.ablation or args.rescale or args.rotate:
+    if args.ablation or args.rescale or args.rotate or args.pipeline:
         layer = synth.make_layer(synth.CONFIGS[args.config], args.seed)
         if args.ablation:
             # the compilations of Sec. 6.2 on the same kernel: every signed term's
@@ -531,6 +618,8 @@ def main():
             extra["rescale"] = dict(time_rescale(layer, dev, args.steps, args.warmup, stream), layer=args.config)
         if args.rotate:
             extra["rotate"] = dict(time_rotate(layer, dev, args.steps, args.warmup, stream), layer=args.config)
+        if args.pipeline:
+            extra["pipeline"] = dict(time_pipeline(layer, dev, args.steps, args.warmup, stream), layer=args.config)
     # each layer's raw-term multiply-adds against the register-only rate
     mb = time_mac_microbench(stream)
     for r in records:
