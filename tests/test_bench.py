@@ -1,4 +1,5 @@
-"""CPU checks of bench.py's contract: one GPU only, and the CPU baseline's fields."""
+"""Checks of bench.py: one GPU only, the CPU baseline's fields, the roofline bytes
+(CPU), and the layer-step timing path (GPU)."""
 import os
 import subprocess
 import sys
@@ -34,3 +35,25 @@ def test_algorithmic_bytes_match_the_roofline_formula():
     for name in ("vgg11", "vit768", "bert_ffn"):
         layer = synth.make_layer(synth.CONFIGS[name], 1)
         assert synth.algorithmic_bytes(layer) == 8 * layer.L * layer.N * (2 * layer.n_in + layer.n_pm + 2 * layer.n_out)
+
+
+@pytest.mark.gpu
+def test_layer_step_timing_runs():
+    """bench.time_pipeline on the Tiny layer (63 rotations at N = 2^12, the
+    weighted sum, the rescale): the eager and the HIP-graph timings exist and
+    the stages add up to the step."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import bench
+    import synth
+    import paper_2609_35352_amd as fiona
+    fiona.lib()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=dev)
+    rec = bench.time_pipeline(synth.make_layer(synth.CONFIGS["tiny"], 1), dev, 3, 1, stream)
+    assert rec["rotations"] == 63
+    for k in ("rotate_ms", "weighted_sum_ms", "rescale_ms", "step_ms", "graph_step_ms"):
+        assert rec[k] > 0, k
+    parts = rec["rotate_ms"] + rec["weighted_sum_ms"] + rec["rescale_ms"]
+    assert abs(parts - rec["step_ms"]) <= 0.25 * rec["step_ms"] + 0.05
