@@ -487,8 +487,8 @@ def time_mac_microbench(stream, blocks=2048, chunks=200, reps=5):
 
 
 def time_streams(stream, gib=4, reps=5):
-    """Measured HBM ceilings: a plain contiguous read and a plain copy of
-    `gib` GiB (best grid of four), next to the 8 TB/s spec."""
+    """Measured HBM ceilings: a plain contiguous read, a plain copy and a plain
+    write of `gib` GiB (best grid of four), next to the 8 TB/s spec."""
     import torch
     import paper_2609_35352_amd as fiona
 
@@ -497,11 +497,12 @@ def time_streams(stream, gib=4, reps=5):
     dst = torch.empty_like(src)
     sink = torch.empty(1 << 15, dtype=torch.int64, device="cuda:0")
     out = {}
-    for kind in ("read", "copy"):
+    for kind in ("read", "copy", "write"):
         best = None
         for blocks in (2048, 4096, 8192, 16384):
-            run = (lambda: fiona.stream_read(src, blocks, sink, stream=stream)) if kind == "read" else \
-                (lambda: fiona.stream_copy(src, dst, blocks, stream=stream))
+            run = {"read": lambda: fiona.stream_read(src, blocks, sink, stream=stream),
+                   "copy": lambda: fiona.stream_copy(src, dst, blocks, stream=stream),
+                   "write": lambda: fiona.stream_write(dst, blocks, stream=stream)}[kind]
             nbytes = run()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -514,7 +515,7 @@ def time_streams(stream, gib=4, reps=5):
             if best is None or gbs > best[0]:
                 best = (gbs, blocks)
         out[kind] = {"GBps": round(best[0], 1), "frac_of_spec": round(best[0] / HBM_PEAK_GBS, 4),
-                     "workgroups": best[1], "bytes": n * 8 * (1 if kind == "read" else 2)}
+                     "workgroups": best[1], "bytes": n * 8 * (2 if kind == "copy" else 1)}
     del src, dst, sink
     torch.cuda.empty_cache()
     out["spec_GBps"] = HBM_PEAK_GBS
@@ -530,7 +531,7 @@ def main():
     ap.add_argument("--layers", default=",".join(LAYERS),
                     help="comma-separated layers to time ('none': only the --ablation/--rescale/--rotate steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-streams", action="store_true", help="skip the read and copy ceilings")
+    ap.add_argument("--no-streams", action="store_true", help="skip the read, copy and write ceilings")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--config", default="vgg11", help="the layer of --ablation, --rescale and --rotate")
     ap.add_argument("--rotate", action="store_true",

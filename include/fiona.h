@@ -429,18 +429,21 @@ uint64_t fiona_mac_microbench_words(uint32_t blocks, uint32_t chunks);
 
 /*
  * Measurement helpers (not part of the weighted sum): the HBM bandwidth of a
- * plain contiguous read and of a plain copy, the ceilings the kernels' rates
- * are set against.  Grid-stride loops over 16-byte words on blocks
- * workgroups of 256 threads, nontemporal accesses.
+ * plain contiguous read, of a plain copy and of a plain write, the ceilings
+ * the kernels' rates are set against.  Grid-stride loops over 16-byte words
+ * on blocks workgroups of 256 threads, nontemporal accesses.
  * fiona_stream_read: reads words (even) uint64 words of src (device, 16-byte
  *   aligned) and writes one word per workgroup to sink (device, blocks words).
  * fiona_stream_copy: dst[i] = src[i] for words (even) words (device, 16-byte
  *   aligned, not overlapping).
+ * fiona_stream_write: writes words (even) words of dst (device, 16-byte
+ *   aligned) with a pattern of the slot index; reads nothing.
  * Asynchronous on stream; allocate nothing.  Errors: FIONA_ERR_ARG,
  * FIONA_ERR_ALIGN, FIONA_ERR_ALIAS (copy), FIONA_ERR_HIP.
  */
 int fiona_stream_read(const uint64_t *src, uint64_t words, uint32_t blocks, uint64_t *sink, hipStream_t stream);
 int fiona_stream_copy(const uint64_t *src, uint64_t *dst, uint64_t words, uint32_t blocks, hipStream_t stream);
+int fiona_stream_write(uint64_t *dst, uint64_t words, uint32_t blocks, hipStream_t stream);
 
 /*
  * Checking helper (no device needed): replays the memory accesses of one

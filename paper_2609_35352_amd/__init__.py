@@ -412,6 +412,17 @@ def stream_copy(src_t, dst_t, blocks: int, stream=None) -> int:
     return 2 * src_t.numel() * 8
 
 
+def stream_write(dst_t, blocks: int, stream=None) -> int:
+    """fiona_stream_write over all of dst_t (8-byte elements, an even count);
+    returns the bytes written."""
+    L_ = lib()
+    L_.fiona_stream_write.restype = ctypes.c_int
+    L_.fiona_stream_write.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p]
+    _check(L_.fiona_stream_write(_dptr(dst_t, "dst", 8), dst_t.numel(), int(blocks), _stream_handle(stream)),
+           "fiona_stream_write")
+    return dst_t.numel() * 8
+
+
 def plan_check_inputs(plan: Plan, signs, scales, x=None, pt=None) -> int:
     """fiona_plan_check_inputs on host arrays (NumPy): signs int8 [n_member],
     scales uint64 [n_scale], x uint64 [n_in][2][L][N] or None, pt uint64 rows at

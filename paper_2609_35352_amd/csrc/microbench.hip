@@ -100,6 +100,19 @@ __global__ void __launch_bounds__(kMicroThreads) stream_copy_kernel(const sv4 *_
   }
 }
 
+// Every 16-byte slot of dst gets (seed, seed + slot, ...): a write-only stream.
+__global__ void __launch_bounds__(kMicroThreads) stream_write_kernel(sv4 *__restrict__ dst, uint64_t n16,
+                                                                     uint32_t seed) {
+  const uint64_t step = (uint64_t)gridDim.x * kMicroThreads * 4;
+  for (uint64_t i = (uint64_t)blockIdx.x * kMicroThreads * 4 + threadIdx.x; i < n16; i += step) {
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) {
+      const uint64_t j = i + u * kMicroThreads;
+      if (j < n16) __builtin_nontemporal_store((sv4){seed, (uint32_t)j, (uint32_t)(j >> 32), seed ^ u}, dst + j);
+    }
+  }
+}
+
 }  // namespace fiona
 
 extern "C" {
@@ -119,6 +132,14 @@ int fiona_stream_copy(const uint64_t *src, uint64_t *dst, uint64_t words, uint32
   if (a < b + words * 8 && b < a + words * 8) return FIONA_ERR_ALIAS;
   hipLaunchKernelGGL(fiona::stream_copy_kernel, dim3(blocks), dim3(fiona::kMicroThreads), 0, stream,
                      (const fiona::sv4 *)src, (fiona::sv4 *)dst, words / 2);
+  return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
+}
+
+int fiona_stream_write(uint64_t *dst, uint64_t words, uint32_t blocks, hipStream_t stream) {
+  if (!dst || blocks == 0 || words == 0 || (words & 1u)) return FIONA_ERR_ARG;
+  if ((uintptr_t)dst & 15u) return FIONA_ERR_ALIGN;
+  hipLaunchKernelGGL(fiona::stream_write_kernel, dim3(blocks), dim3(fiona::kMicroThreads), 0, stream,
+                     (fiona::sv4 *)dst, words / 2, 0x9E3779B9u);
   return hipGetLastError() == hipSuccess ? FIONA_OK : FIONA_ERR_HIP;
 }
 
